@@ -1,0 +1,239 @@
+"""Benchmark: GASLoC rounds on one MI355X through libgasloc.so.
+
+One step = one whole round of the hot path on resident synthetic replicas:
+H_i masked local AdamW steps, the fused gossip round (pseudo-gradient, outer
+Nesterov step, neighbour mix, consensus momentum, consensus-error partials),
+its fp64 finalize and the consensus-error readback.  `value` is
+replica-param updates per second, n * P / (seconds per round).
+
+Prints ONE JSON line.  Per-kernel durations come from HIP events recorded on
+the library's stream around every call inside the timed region.
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, AMD specification
+METRIC = "replica-param updates/s per gossip round; achieved HBM GB/s vs peak"
+DEFAULT_WORKLOAD = "onepeer-exp-n16-p350m"
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_11081_amd", "csrc", "kernels.hip")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernels_sha():
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def param_bytes(dtype):
+    return 2 if dtype == "bf16" else 4
+
+
+def adamw_bytes_per_rp(sp):
+    # read y (or x), g, m, v; write y, m, v
+    return 2 * sp + 20
+
+
+def gossip_bytes_per_rp(sp, gamma, stepped=True, with_u=True):
+    # read x, y (stepped workers), u, zp (gamma); write x, u, zp (gamma)
+    b = sp + sp  # x read + x write
+    if stepped:
+        b += sp
+    if with_u:
+        b += 8
+    if gamma != 0.0:
+        b += 8
+    return b
+
+
+def read_traffic(kernel, workload):
+    """HBM bytes per dispatch from a committed rocprofv3 --pmc summary, or None
+    if absent or taken on a different kernel source."""
+    path = os.path.join(ROOT, "profiles", "%s_%s_pmc.md" % (kernel, workload))
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"traffic_bytes_per_dispatch:\s*([0-9.eE+]+)\s+kernels_sha:\s*([0-9a-f]+)", text)
+    if not m or m.group(2) != kernels_sha():
+        return None
+    return float(m.group(1))
+
+
+def cpu_baseline(w, H_i, columns):
+    """The oracle as it stands, single-threaded, on `columns` columns of the
+    same workload: one full round (all local steps, gossip, consensus error)."""
+    import numpy as np
+
+    import gasloc_inputs as gi
+    import oracle
+
+    hp = oracle.OracleHParams(beta1=gi.BETA1, beta2=gi.BETA2, eps=gi.EPS, weight_decay=gi.WEIGHT_DECAY,
+                              outer_lr=gi.OUTER_LR, outer_momentum=gi.OUTER_MOMENTUM,
+                              nesterov=True, consensus_momentum=w.gamma)
+    o = oracle.Oracle(w.n, columns, hp, topology=w.topology, seed=gi.SEED_TOPOLOGY, degree=w.degree,
+                      precision="f32", param_dtype=w.param_dtype)
+    rng = np.random.default_rng(0)
+    x0 = (rng.standard_normal(columns) * 0.02).astype(np.float32)
+    o.set_params(x0)
+    g = (rng.standard_normal((w.n, columns)) + gi.worker_means(w.n)[:, None]).astype(np.float32)
+    t0 = time.perf_counter()
+    for h in range(int(H_i.max())):
+        o.local_step(g, gi.LOCAL_LR, (H_i > h).astype(np.uint8))
+    o.gossip_round(0)
+    o.consensus_error()
+    dt = time.perf_counter() - t0
+    return {"value": w.n * columns / dt, "unit": "replica-param updates/s", "cores": 1, "kind": "oracle",
+            "sample": "%d of %d columns x %d workers, one round (%d local steps + gossip + CE), "
+                      "plain C oracle (fp32 build, -O2, single thread): %.2f s"
+                      % (columns, w.P, w.n, int(H_i.max()), dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--cpu-columns", type=int, default=1 << 23)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-gb", type=float, default=8.0, help="size of the copy probe (GB read)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: every replica of the round lives on a single MI355X; "
+              "runs on %d GPUs are not part of this build" % max(args.gpus, 1), file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import gasloc_inputs as gi
+    import paper_2606_11081_amd as g
+
+    w = gi.WORKLOADS[args.workload]
+    H_i = gi.local_steps(w)
+    masks = gi.active_masks(H_i)
+    sp = param_bytes(w.param_dtype)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    log("bench: %s  (n=%d P=%d %s H=%s gamma=%g)" % (w.name, w.n, w.P, w.param_dtype,
+                                                    "U{%d..%d}" % w.hetero_H if w.hetero_H else w.H, w.gamma))
+
+    lib = g.GASLoC(w.n, w.P, topology=w.topology, seed=gi.SEED_TOPOLOGY, degree=w.degree,
+                   param_dtype=w.param_dtype, beta1=gi.BETA1, beta2=gi.BETA2, eps=gi.EPS,
+                   weight_decay=gi.WEIGHT_DECAY, outer_lr=gi.OUTER_LR, outer_momentum=gi.OUTER_MOMENTUM,
+                   outer_nesterov=True, consensus_momentum=w.gamma)
+    lib.set_params(gi.make_x0(w.P, device=dev))
+    # one resident gradient batch (stand-in for backpropagated gradients)
+    grads = torch.empty((w.n, lib.ld), dtype=torch.float32, device=dev)
+    gi.fill_grads(grads, gi.worker_means(w.n), 0)
+    stream = lib.stream
+    torch.cuda.synchronize()
+
+    def one_round(t, ev=None):
+        for h, act in enumerate(masks):
+            if ev is not None:
+                ev["adam"].append((torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+                                   int(act.sum())))
+                ev["adam"][-1][0].record(stream)
+            lib.local_step(grads, gi.LOCAL_LR, act)
+            if ev is not None:
+                ev["adam"][-1][1].record(stream)
+        if ev is not None:
+            ev["gossip"].append((torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)))
+            ev["gossip"][-1][0].record(stream)
+        lib.gossip_round(t)
+        if ev is not None:
+            ev["gossip"][-1][1].record(stream)
+        return lib.consensus_error()
+
+    for t in range(args.warmup):
+        one_round(t)
+    torch.cuda.synchronize()
+
+    ev = {"adam": [], "gossip": []}
+    ces = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        ces.append(one_round(args.warmup + s, ev))
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_step = elapsed / args.steps * 1e3
+
+    adam_ms = [a.elapsed_time(b) for a, b, _ in ev["adam"]]
+    adam_rp = [k * w.P for _, _, k in ev["adam"]]
+    gossip_ms = [a.elapsed_time(b) for a, b in ev["gossip"]]
+    adam_bytes = adamw_bytes_per_rp(sp)
+    gossip_bytes = gossip_bytes_per_rp(sp, w.gamma)
+    adam_gbps = sum(r * adam_bytes for r in adam_rp) / (sum(adam_ms) * 1e-3) / 1e9
+    gossip_gbps = w.n * w.P * gossip_bytes / (np.mean(gossip_ms) * 1e-3) / 1e9
+    adam_total, gossip_total = sum(adam_ms), sum(gossip_ms)
+
+    # copy probe: a plain device copy of known size, same run
+    copy_elems = int(args.copy_gb * 1e9 / 4)
+    src = torch.empty(copy_elems, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record(stream)
+    for _ in range(5):
+        dst.copy_(src)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbps = 2 * copy_elems * 4 * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    del src, dst
+
+    if adam_total >= gossip_total and adam_ms:
+        dom, dom_bytes = "k_local_adamw", np.mean([r * adam_bytes for r in adam_rp])
+        dom_ms = float(np.mean(adam_ms))
+    else:
+        dom, dom_bytes, dom_ms = "k_gossip_round", w.n * w.P * gossip_bytes, float(np.mean(gossip_ms))
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
+                "traffic": read_traffic(dom, w.name),
+                "algorithmic_bytes_per_launch": int(dom_bytes), "avg_launch_ms": round(dom_ms, 4)}
+    gossip_rp = w.n * w.P / (np.mean(gossip_ms) * 1e-3)
+    out = {
+        "metric": METRIC,
+        "value": w.n * w.P / (ms_step * 1e-3),
+        "unit": "replica-param updates/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.param_dtype, "data": "synthetic",
+        "config": {"workload": w.name, "n": w.n, "P": w.P, "topology": w.topology,
+                   "local_steps": "U{%d..%d}" % w.hetero_H if w.hetero_H else w.H,
+                   "gamma": w.gamma, "param_dtype": w.param_dtype, "state_dtype": "f32"},
+        "roofline": roofline,
+        "gossip_round": {"rp_updates_per_s": gossip_rp, "ms": round(float(np.mean(gossip_ms)), 4),
+                         "GBps": round(gossip_gbps, 1), "frac_of_peak": round(gossip_gbps / PEAK_HBM_GBPS, 4),
+                         "bytes_per_rp": gossip_bytes, "traffic": read_traffic("k_gossip_round", w.name)},
+        "local_adamw": {"ms_per_launch": round(float(np.mean(adam_ms)), 4), "GBps": round(adam_gbps, 1),
+                        "frac_of_peak": round(adam_gbps / PEAK_HBM_GBPS, 4), "bytes_per_rp": adam_bytes,
+                        "launches_per_round": len(masks)},
+        "copy_probe_GBps": round(copy_gbps, 1),
+        "consensus_error_last": ces[-1],
+    }
+    lib.close()
+    del grads
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        log("bench: timing the oracle on %d columns" % args.cpu_columns)
+        out["cpu_baseline"] = cpu_baseline(w, H_i, min(args.cpu_columns, w.P))
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

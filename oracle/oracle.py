@@ -261,8 +261,12 @@ class Oracle:
             raise ValueError("oracle gossip_round rejected its arguments")
         self.rounds_done += 1
 
-    def consensus_error(self):
-        return self.L.orc_consensus_error(self.n, self.P, self.P, self.pcode, _ptr(self.x))
+    def consensus_error(self, cols=None):
+        """||pi x||^2 over all columns, or over the column slice/index array `cols`."""
+        if cols is None:
+            return self.L.orc_consensus_error(self.n, self.P, self.P, self.pcode, _ptr(self.x))
+        sub = np.ascontiguousarray(self.x[:, cols])
+        return self.L.orc_consensus_error(self.n, sub.shape[1], sub.shape[1], self.pcode, _ptr(sub))
 
     def replica_mean(self):
         out = np.zeros(self.P, dtype=self.pdt)

@@ -1,0 +1,83 @@
+// Internal interfaces between the C ABI (runtime.cpp), the schedule generator
+// (topology.cpp) and the HIP kernels (kernels.hip).  Not installed.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+
+#include <cstdint>
+#include <string>
+
+#include "gasloc.h"
+
+namespace gasloc {
+
+constexpr int kMaxReplicas = 64;
+
+bool make_topology(const gasloc_topology& topo, int n, uint64_t t, int32_t* row_ptr, int32_t* col,
+                   float* val, int32_t cap, int32_t* nnz, std::string* err);
+
+// ---------------------------------------------------------------------------
+// kernel arguments (passed by value)
+// ---------------------------------------------------------------------------
+
+// One local AdamW step over the active workers.  Slot s of the launch works
+// on worker rep[s]; bit s of from_x says that worker's live iterate is still
+// the round anchor x (first step after a round), so the step reads x.
+struct AdamArgs {
+  const void* x;
+  void* y;
+  float* m;
+  float* v;
+  const float* g;
+  int64_t ld, gld, P;
+  float c_wd, b1, omb1, b2, omb2, eps;
+  int32_t n_active;
+  uint64_t from_x;
+  int32_t rep[kMaxReplicas];
+  float s1[kMaxReplicas];  // lr / (1 - b1^k)
+  float c2[kMaxReplicas];  // sqrt(1 - b2^k)
+};
+
+// One gossip round; the consensus-error partial of every workgroup goes to
+// partials[blockIdx.x].
+struct GossipArgs {
+  void* x;
+  const void* y;
+  float* u;
+  float* zp;
+  const int32_t* row_ptr;
+  const int32_t* col;
+  const float* val;
+  double* partials;
+  int64_t ld, P;
+  int32_t n, nnz;
+  float mu, eta, gamma;
+  int32_t nesterov;
+  int32_t use_u;        // outer momentum buffer present (mu != 0)
+  int32_t apply_gamma;  // gamma term of Eq. 2 (not in the first round)
+  int32_t store_zp;     // keep z for the next round's gamma term
+  uint64_t stepped;     // bit i: worker i took local steps since the last round
+};
+
+struct LaunchShape {
+  int vec;      // columns per thread per iteration (1, 2 or 4)
+  int threads;  // workgroup size
+  int blocks;   // workgroups (grid-stride loop inside)
+};
+
+// Launchers: enqueue on `stream`, return the launch status.
+hipError_t launch_local_adamw(const AdamArgs& a, int dtype, int blocks_per_worker, hipStream_t stream);
+hipError_t launch_gossip_round(const GossipArgs& a, int dtype, const LaunchShape& shape,
+                               hipStream_t stream);
+hipError_t launch_consensus_error(const void* x, int dtype, int64_t ld, int n, int64_t p_begin,
+                                  int64_t p_end, double* partials, int blocks, hipStream_t stream);
+hipError_t launch_finalize(const double* partials, int count, double* out, hipStream_t stream);
+hipError_t launch_replica_mean(const void* x, int dtype, int64_t ld, int n, int64_t P, void* out,
+                               int blocks, hipStream_t stream);
+
+// Dynamic LDS bytes one workgroup of the gossip kernel needs (z slots of
+// every thread plus the staged CSR); the kernel also uses kStaticLds bytes.
+size_t gossip_lds_bytes(int n, int nnz, const LaunchShape& shape);
+constexpr size_t kStaticLds = 1024 / 64 * sizeof(double);
+
+}  // namespace gasloc

@@ -1,0 +1,447 @@
+// HIP kernels of the GASLoC round for CDNA4 (gfx950).
+//
+// Every kernel here streams [n, P] buffers once: the path is HBM-bandwidth
+// bound (well under 2 flop per byte), so the kernels use the vector ALU only
+// (no MFMA), 16-byte-per-lane loads and stores where the dtype allows, and a
+// grid-stride loop over column groups.
+//
+// Floating-point contract: no contraction (each product and sum is rounded
+// on its own), correctly rounded fp32 division and square root (HIP's
+// default), fp64 for every reduction.
+#pragma clang fp contract(off)
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "internal.h"
+
+namespace gasloc {
+namespace {
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// parameter storage
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
+
+// binary32 -> bfloat16, round to nearest, ties to even; NaN stays a quiet NaN
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+// Load V consecutive fp32 values; `cnt` < V only for the ragged last group of
+// a row, which is read element by element.
+template <int V>
+__device__ __forceinline__ void load_f32(const float* p, int cnt, float (&o)[V]) {
+  if (cnt == V) {
+    if constexpr (V == 4) {
+      const float4 t = *reinterpret_cast<const float4*>(p);
+      o[0] = t.x; o[1] = t.y; o[2] = t.z; o[3] = t.w;
+    } else if constexpr (V == 2) {
+      const float2 t = *reinterpret_cast<const float2*>(p);
+      o[0] = t.x; o[1] = t.y;
+    } else {
+      o[0] = *p;
+    }
+  } else {
+#pragma unroll
+    for (int c = 0; c < V; ++c) o[c] = c < cnt ? p[c] : 0.0f;
+  }
+}
+
+template <int V>
+__device__ __forceinline__ void store_f32(float* p, int cnt, const float (&o)[V]) {
+  if (cnt == V) {
+    if constexpr (V == 4) {
+      *reinterpret_cast<float4*>(p) = make_float4(o[0], o[1], o[2], o[3]);
+    } else if constexpr (V == 2) {
+      *reinterpret_cast<float2*>(p) = make_float2(o[0], o[1]);
+    } else {
+      *p = o[0];
+    }
+  } else {
+#pragma unroll
+    for (int c = 0; c < V; ++c)
+      if (c < cnt) p[c] = o[c];
+  }
+}
+
+template <int V>
+__device__ __forceinline__ void load_bf16(const uint16_t* p, int cnt, float (&o)[V]) {
+  if (cnt == V) {
+    if constexpr (V == 4) {
+      const uint2 t = *reinterpret_cast<const uint2*>(p);
+      o[0] = bf16_to_f32(t.x & 0xffffu); o[1] = bf16_to_f32(t.x >> 16);
+      o[2] = bf16_to_f32(t.y & 0xffffu); o[3] = bf16_to_f32(t.y >> 16);
+    } else if constexpr (V == 2) {
+      const uint32_t t = *reinterpret_cast<const uint32_t*>(p);
+      o[0] = bf16_to_f32(t & 0xffffu); o[1] = bf16_to_f32(t >> 16);
+    } else {
+      o[0] = bf16_to_f32(*p);
+    }
+  } else {
+#pragma unroll
+    for (int c = 0; c < V; ++c) o[c] = c < cnt ? bf16_to_f32(p[c]) : 0.0f;
+  }
+}
+
+// Rounds to bf16, stores, and returns the stored values as fp32 in `kept`.
+template <int V>
+__device__ __forceinline__ void store_bf16(uint16_t* p, int cnt, const float (&o)[V], float (&kept)[V]) {
+  uint32_t h[V];
+#pragma unroll
+  for (int c = 0; c < V; ++c) {
+    h[c] = f32_to_bf16(o[c]);
+    kept[c] = bf16_to_f32(h[c]);
+  }
+  if (cnt == V) {
+    if constexpr (V == 4) {
+      *reinterpret_cast<uint2*>(p) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+    } else if constexpr (V == 2) {
+      *reinterpret_cast<uint32_t*>(p) = h[0] | (h[1] << 16);
+    } else {
+      *p = static_cast<uint16_t>(h[0]);
+    }
+  } else {
+#pragma unroll
+    for (int c = 0; c < V; ++c)
+      if (c < cnt) p[c] = static_cast<uint16_t>(h[c]);
+  }
+}
+
+template <int DT, int V>
+__device__ __forceinline__ void load_params(const void* base, int64_t idx, int cnt, float (&o)[V]) {
+  if constexpr (DT == GASLOC_BF16)
+    load_bf16<V>(static_cast<const uint16_t*>(base) + idx, cnt, o);
+  else
+    load_f32<V>(static_cast<const float*>(base) + idx, cnt, o);
+}
+
+template <int DT, int V>
+__device__ __forceinline__ void store_params(void* base, int64_t idx, int cnt, const float (&o)[V],
+                                             float (&kept)[V]) {
+  if constexpr (DT == GASLOC_BF16) {
+    store_bf16<V>(static_cast<uint16_t*>(base) + idx, cnt, o, kept);
+  } else {
+    store_f32<V>(static_cast<float*>(base) + idx, cnt, o);
+#pragma unroll
+    for (int c = 0; c < V; ++c) kept[c] = o[c];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// reductions: fixed-order wave shuffle, then the waves of the workgroup
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_down(v, off, kWave);
+  return v;
+}
+
+// Sum of `v` over the workgroup, valid in thread 0.
+__device__ __forceinline__ double block_sum(double v) {
+  __shared__ double wave_part[1024 / kWave];
+  v = wave_sum(v);
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  if (lane == 0) wave_part[wave] = v;
+  __syncthreads();
+  double total = 0.0;
+  if (threadIdx.x == 0) {
+    const int waves = (blockDim.x + kWave - 1) / kWave;
+    for (int w = 0; w < waves; ++w) total += wave_part[w];
+  }
+  return total;
+}
+
+// ---------------------------------------------------------------------------
+// a1: local AdamW step
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float adamw_element(float y, float g, float& m, float& v, float c_wd,
+                                               float b1, float omb1, float b2, float omb2,
+                                               float eps, float s1, float c2) {
+  const float w = y * c_wd;
+  m = b1 * m + omb1 * g;
+  v = b2 * v + omb2 * (g * g);
+  const float d = sqrtf(v) / c2 + eps;
+  return w - s1 * (m / d);
+}
+
+// grid: (blocks_per_worker, n_active); slot blockIdx.y updates worker rep[slot].
+template <int DT>
+__global__ __launch_bounds__(256) void k_local_adamw(AdamArgs a) {
+  const int slot = blockIdx.y;
+  const int r = a.rep[slot];
+  const bool from_x = (a.from_x >> slot) & 1ull;
+  const float s1 = a.s1[slot], c2 = a.c2[slot];
+  const int64_t row = static_cast<int64_t>(r) * a.ld;
+  const int64_t grow = static_cast<int64_t>(r) * a.gld;
+  const void* src = from_x ? a.x : a.y;
+  constexpr int V = 4;
+  const int64_t groups = (a.P + V - 1) / V;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  for (int64_t gi = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; gi < groups;
+       gi += stride) {
+    const int64_t p = gi * V;
+    const int cnt = static_cast<int>(a.P - p < V ? a.P - p : V);
+    float w[V], g[V], m[V], v[V], out[V], kept[V];
+    load_params<DT, V>(src, row + p, cnt, w);
+    load_f32<V>(a.g + grow + p, cnt, g);
+    load_f32<V>(a.m + row + p, cnt, m);
+    load_f32<V>(a.v + row + p, cnt, v);
+#pragma unroll
+    for (int c = 0; c < V; ++c)
+      out[c] = adamw_element(w[c], g[c], m[c], v[c], a.c_wd, a.b1, a.omb1, a.b2, a.omb2, a.eps, s1, c2);
+    store_params<DT, V>(a.y, row + p, cnt, out, kept);
+    store_f32<V>(a.m + row + p, cnt, m);
+    store_f32<V>(a.v + row + p, cnt, v);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// a2-a5: pseudo-gradient, outer step, neighbour mix, consensus momentum and
+// the consensus-error partial, fused.  A thread owns V consecutive columns
+// of *every* worker, so each element of x, y, u, zp is read and written
+// exactly once and the in-place updates cannot race.  The post-outer
+// iterates z of all n workers at those columns sit in LDS (this thread's
+// private slots, so no barrier is needed between writing and gathering);
+// the CSR is staged in LDS once per workgroup.
+// ---------------------------------------------------------------------------
+
+struct CsrEntry {
+  int32_t col;
+  float val;
+};
+
+template <int DT, int V>
+__global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int n = a.n;
+  const int nt = blockDim.x;
+  const int tid = threadIdx.x;
+  float* zs = reinterpret_cast<float*>(lds);  // [n][nt][V]
+  const size_t z_bytes = static_cast<size_t>(n) * nt * V * sizeof(float);
+  int32_t* rp = reinterpret_cast<int32_t*>(lds + z_bytes);  // [n + 1]
+  const size_t rp_bytes = (static_cast<size_t>(n + 1) * sizeof(int32_t) + 7) & ~size_t(7);
+  CsrEntry* ent = reinterpret_cast<CsrEntry*>(lds + z_bytes + rp_bytes);  // [nnz]
+
+  const int nnz = a.nnz;
+  for (int k = tid; k <= n; k += nt) rp[k] = a.row_ptr[k];
+  for (int k = tid; k < nnz; k += nt) ent[k] = CsrEntry{a.col[k], a.val[k]};
+  __syncthreads();
+
+  const double inv_n = 1.0 / static_cast<double>(n);
+  const int64_t groups = (a.P + V - 1) / V;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * nt;
+  double ce = 0.0;
+  for (int64_t gi = static_cast<int64_t>(blockIdx.x) * nt + tid; gi < groups; gi += stride) {
+    const int64_t p = gi * V;
+    const int cnt = static_cast<int>(a.P - p < V ? a.P - p : V);
+
+    // phase 1: delta = x - y, outer (Nesterov / heavy-ball) step -> z
+    for (int i = 0; i < n; ++i) {
+      const int64_t e = static_cast<int64_t>(i) * a.ld + p;
+      float xv[V], yv[V], uv[V], z[V];
+      load_params<DT, V>(a.x, e, cnt, xv);
+      if ((a.stepped >> i) & 1ull) {
+        load_params<DT, V>(a.y, e, cnt, yv);
+      } else {
+#pragma unroll
+        for (int c = 0; c < V; ++c) yv[c] = xv[c];
+      }
+      if (a.use_u) {
+        load_f32<V>(a.u + e, cnt, uv);
+      } else {
+#pragma unroll
+        for (int c = 0; c < V; ++c) uv[c] = 0.0f;
+      }
+#pragma unroll
+      for (int c = 0; c < V; ++c) {
+        const float delta = xv[c] - yv[c];
+        uv[c] = a.mu * uv[c] + delta;
+        const float step = a.nesterov ? delta + a.mu * uv[c] : uv[c];
+        z[c] = xv[c] - a.eta * step;
+      }
+      if (a.use_u) store_f32<V>(a.u + e, cnt, uv);
+      float* zslot = zs + (static_cast<size_t>(i) * nt + tid) * V;
+#pragma unroll
+      for (int c = 0; c < V; ++c) zslot[c] = z[c];
+    }
+
+    // phase 2: x_i = sum_k W_ik z_k (+ gamma (z_i - zp_i)), zp_i = z_i,
+    // consensus error of the stored x from shifted fp64 sums
+    double shift[V], s[V], q[V];
+    for (int i = 0; i < n; ++i) {
+      const int64_t e = static_cast<int64_t>(i) * a.ld + p;
+      float acc[V];
+#pragma unroll
+      for (int c = 0; c < V; ++c) acc[c] = 0.0f;
+      const int kb = rp[i], ke = rp[i + 1];
+      for (int k = kb; k < ke; ++k) {
+        const CsrEntry w = ent[k];
+        const float* zj = zs + (static_cast<size_t>(w.col) * nt + tid) * V;
+#pragma unroll
+        for (int c = 0; c < V; ++c) acc[c] = acc[c] + w.val * zj[c];
+      }
+      const float* zi = zs + (static_cast<size_t>(i) * nt + tid) * V;
+      float zcur[V];
+#pragma unroll
+      for (int c = 0; c < V; ++c) zcur[c] = zi[c];
+      if (a.apply_gamma) {
+        float zpv[V];
+        load_f32<V>(a.zp + e, cnt, zpv);
+#pragma unroll
+        for (int c = 0; c < V; ++c) acc[c] = acc[c] + a.gamma * (zcur[c] - zpv[c]);
+      }
+      if (a.store_zp) store_f32<V>(a.zp + e, cnt, zcur);
+      float kept[V];
+      store_params<DT, V>(a.x, e, cnt, acc, kept);
+#pragma unroll
+      for (int c = 0; c < V; ++c) {
+        const double xd = static_cast<double>(kept[c]);
+        if (i == 0) {
+          shift[c] = xd;
+          s[c] = 0.0;
+          q[c] = 0.0;
+        }
+        const double d = xd - shift[c];
+        s[c] += d;
+        q[c] += d * d;
+      }
+    }
+    // sum_i (x_i - xbar)^2 = q - s^2/n with deviations taken from x_0: the
+    // cancellation is bounded because q <= (n + 1) * result
+#pragma unroll
+    for (int c = 0; c < V; ++c)
+      if (c < cnt) ce += q[c] - s[c] * s[c] * inv_n;
+  }
+  const double total = block_sum(ce);
+  if (tid == 0) a.partials[blockIdx.x] = total;
+}
+
+// ---------------------------------------------------------------------------
+// a5 standalone: consensus error of the stored x over columns [p_begin, p_end)
+// ---------------------------------------------------------------------------
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_consensus_error(const void* x, int64_t ld, int n,
+                                                         int64_t p_begin, int64_t p_end,
+                                                         double* partials) {
+  const double inv_n = 1.0 / static_cast<double>(n);
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  double ce = 0.0;
+  for (int64_t p = p_begin + static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; p < p_end;
+       p += stride) {
+    float v[1];
+    load_params<DT, 1>(x, p, 1, v);
+    const double shift = v[0];
+    double s = 0.0, q = 0.0;
+    for (int i = 1; i < n; ++i) {
+      load_params<DT, 1>(x, static_cast<int64_t>(i) * ld + p, 1, v);
+      const double d = static_cast<double>(v[0]) - shift;
+      s += d;
+      q += d * d;
+    }
+    ce += q - s * s * inv_n;
+  }
+  const double total = block_sum(ce);
+  if (threadIdx.x == 0) partials[blockIdx.x] = total;
+}
+
+// Fixed-order sum of `count` partials into *out (one workgroup).
+__global__ __launch_bounds__(256) void k_finalize(const double* partials, int count, double* out) {
+  double v = 0.0;
+  for (int k = threadIdx.x; k < count; k += blockDim.x) v += partials[k];
+  const double total = block_sum(v);
+  if (threadIdx.x == 0) *out = total;
+}
+
+// a6: network average, fp64 sum in worker order, rounded to the param dtype
+template <int DT>
+__global__ __launch_bounds__(256) void k_replica_mean(const void* x, int64_t ld, int n, int64_t P,
+                                                      void* out) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  for (int64_t p = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; p < P; p += stride) {
+    double s = 0.0;
+    for (int i = 0; i < n; ++i) {
+      float v[1];
+      load_params<DT, 1>(x, static_cast<int64_t>(i) * ld + p, 1, v);
+      s += static_cast<double>(v[0]);
+    }
+    const float mean[1] = {static_cast<float>(s / static_cast<double>(n))};
+    float kept[1];
+    store_params<DT, 1>(out, p, 1, mean, kept);
+  }
+}
+
+template <int DT, int V>
+hipError_t launch_gossip_typed(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
+  const size_t lds = gossip_lds_bytes(a.n, a.nnz, s);
+  hipLaunchKernelGGL((k_gossip_round<DT, V>), dim3(s.blocks), dim3(s.threads), lds, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t gossip_lds_bytes(int n, int nnz, const LaunchShape& s) {
+  const size_t z_bytes = static_cast<size_t>(n) * s.threads * s.vec * sizeof(float);
+  const size_t rp_bytes = (static_cast<size_t>(n + 1) * sizeof(int32_t) + 7) & ~size_t(7);
+  const size_t ent_bytes = static_cast<size_t>(nnz) * sizeof(CsrEntry);
+  return z_bytes + rp_bytes + ent_bytes;
+}
+
+hipError_t launch_local_adamw(const AdamArgs& a, int dtype, int blocks_per_worker, hipStream_t stream) {
+  const dim3 grid(blocks_per_worker, a.n_active);
+  if (dtype == GASLOC_BF16)
+    hipLaunchKernelGGL((k_local_adamw<GASLOC_BF16>), grid, dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL((k_local_adamw<GASLOC_F32>), grid, dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gossip_round(const GossipArgs& a, int dtype, const LaunchShape& s, hipStream_t stream) {
+  if (dtype == GASLOC_BF16) {
+    if (s.vec == 4) return launch_gossip_typed<GASLOC_BF16, 4>(a, s, stream);
+    if (s.vec == 2) return launch_gossip_typed<GASLOC_BF16, 2>(a, s, stream);
+    return launch_gossip_typed<GASLOC_BF16, 1>(a, s, stream);
+  }
+  if (s.vec == 4) return launch_gossip_typed<GASLOC_F32, 4>(a, s, stream);
+  if (s.vec == 2) return launch_gossip_typed<GASLOC_F32, 2>(a, s, stream);
+  return launch_gossip_typed<GASLOC_F32, 1>(a, s, stream);
+}
+
+hipError_t launch_consensus_error(const void* x, int dtype, int64_t ld, int n, int64_t p_begin,
+                                  int64_t p_end, double* partials, int blocks, hipStream_t stream) {
+  if (dtype == GASLOC_BF16)
+    hipLaunchKernelGGL((k_consensus_error<GASLOC_BF16>), dim3(blocks), dim3(256), 0, stream, x, ld, n,
+                       p_begin, p_end, partials);
+  else
+    hipLaunchKernelGGL((k_consensus_error<GASLOC_F32>), dim3(blocks), dim3(256), 0, stream, x, ld, n,
+                       p_begin, p_end, partials);
+  return hipGetLastError();
+}
+
+hipError_t launch_finalize(const double* partials, int count, double* out, hipStream_t stream) {
+  hipLaunchKernelGGL(k_finalize, dim3(1), dim3(256), 0, stream, partials, count, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_replica_mean(const void* x, int dtype, int64_t ld, int n, int64_t P, void* out,
+                               int blocks, hipStream_t stream) {
+  if (dtype == GASLOC_BF16)
+    hipLaunchKernelGGL((k_replica_mean<GASLOC_BF16>), dim3(blocks), dim3(256), 0, stream, x, ld, n, P,
+                       out);
+  else
+    hipLaunchKernelGGL((k_replica_mean<GASLOC_F32>), dim3(blocks), dim3(256), 0, stream, x, ld, n, P,
+                       out);
+  return hipGetLastError();
+}
+
+}  // namespace gasloc

@@ -1,0 +1,560 @@
+// C ABI of libgasloc.so: argument checks, per-context state, scalar
+// precompute, CSR staging and kernel launches.  See include/gasloc.h for the
+// contract of every call.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "gasloc.h"
+#include "internal.h"
+
+using gasloc::kMaxReplicas;
+
+namespace {
+
+constexpr int kStageSlots = 4;      // pinned CSR staging slots, reused round-robin
+constexpr int kMaxGridBlocks = 16384;
+
+thread_local std::string g_thread_error;
+
+std::string format(const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  return std::string(buf);
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t param_bytes(int dtype) { return dtype == GASLOC_BF16 ? 2 : 4; }
+
+// Byte layout of one staged CSR: row_ptr[n+1] | col[n*n] | val[n*n].
+size_t csr_stage_bytes(int n) {
+  return sizeof(int32_t) * static_cast<size_t>(n + 1) + (sizeof(int32_t) + sizeof(float)) * n * n;
+}
+
+}  // namespace
+
+struct gasloc_ctx {
+  int n = 0;
+  int64_t P = 0;
+  gasloc_topology topo{};
+  gasloc_hparams hp{};
+  gasloc_buffers buf{};
+  hipStream_t stream = nullptr;
+  int device = 0;
+  int cus = 0;
+
+  std::vector<int64_t> k;         // AdamW step count per worker
+  std::vector<uint8_t> stepped;   // local steps taken since the last round
+  int64_t rounds_done = 0;
+  bool ce_current = false;        // d_ce holds the consensus error of the stored x
+  bool failed = false;
+
+  unsigned char* d_csr = nullptr;  // device copy of the round's CSR
+  unsigned char* h_stage[kStageSlots] = {};
+  hipEvent_t stage_done[kStageSlots] = {};
+  bool stage_used[kStageSlots] = {};
+  int stage_next = 0;
+  double* d_partials = nullptr;
+  int partial_cap = 0;
+  double* d_ce = nullptr;
+  double* h_ce = nullptr;
+
+  int adam_blocks_total = 0;
+  int reduce_blocks = 0;
+  size_t lds_per_block_max = 0;
+  size_t lds_per_cu = 0;
+
+  std::string err;
+  // scratch for generated CSRs
+  std::vector<int32_t> row_ptr, col;
+  std::vector<float> val;
+};
+
+namespace {
+
+gasloc_status fail(gasloc_ctx* ctx, gasloc_status st, const std::string& msg) {
+  if (ctx) {
+    ctx->err = msg;
+    if (st == GASLOC_EDEVICE) ctx->failed = true;
+  } else {
+    g_thread_error = msg;
+  }
+  return st;
+}
+
+gasloc_status hip_fail(gasloc_ctx* ctx, hipError_t e, const char* what) {
+  return fail(ctx, GASLOC_EDEVICE, format("%s: %s", what, hipGetErrorString(e)));
+}
+
+#define HIP_TRY(ctx, call)                                   \
+  do {                                                       \
+    hipError_t e_ = (call);                                  \
+    if (e_ != hipSuccess) return hip_fail((ctx), e_, #call); \
+  } while (0)
+
+// Makes ctx->device current for the duration of an ABI call.
+class DeviceGuard {
+ public:
+  explicit DeviceGuard(int device) {
+    if (hipGetDevice(&prev_) == hipSuccess && prev_ != device) {
+      if (hipSetDevice(device) == hipSuccess) restore_ = true;
+    }
+  }
+  ~DeviceGuard() {
+    if (restore_) (void)hipSetDevice(prev_);
+  }
+
+ private:
+  int prev_ = -1;
+  bool restore_ = false;
+};
+
+bool finite(float v) { return std::isfinite(v); }
+
+std::string check_hparams(const gasloc_hparams& h) {
+  if (!(finite(h.beta1) && h.beta1 >= 0.0f && h.beta1 < 1.0f)) return "beta1 must be in [0, 1)";
+  if (!(finite(h.beta2) && h.beta2 >= 0.0f && h.beta2 < 1.0f)) return "beta2 must be in [0, 1)";
+  if (!(finite(h.eps) && h.eps > 0.0f)) return "eps must be finite and > 0";
+  if (!(finite(h.weight_decay) && h.weight_decay >= 0.0f)) return "weight_decay must be finite and >= 0";
+  if (!(finite(h.outer_lr) && h.outer_lr > 0.0f)) return "outer_lr must be finite and > 0";
+  if (!(finite(h.outer_momentum) && h.outer_momentum >= 0.0f && h.outer_momentum < 1.0f))
+    return "outer_momentum must be in [0, 1)";
+  if (h.outer_nesterov != 0 && h.outer_nesterov != 1) return "outer_nesterov must be 0 or 1";
+  if (!(finite(h.consensus_momentum) && h.consensus_momentum >= 0.0f && h.consensus_momentum < 1.0f))
+    return "consensus_momentum must be in [0, 1)";
+  if (h.param_dtype != GASLOC_F32 && h.param_dtype != GASLOC_BF16) return "param_dtype must be F32 or BF16";
+  return "";
+}
+
+std::string check_csr(const gasloc_csr& W, int n) {
+  if (W.n != n) return format("CSR has n=%d, context has n=%d", W.n, n);
+  if (!W.row_ptr || (W.nnz > 0 && (!W.col || !W.val))) return "CSR arrays must not be NULL";
+  if (W.nnz < n || W.nnz > n * n) return format("CSR nnz=%d outside [n, n*n]", W.nnz);
+  if (W.row_ptr[0] != 0 || W.row_ptr[n] != W.nnz) return "CSR row_ptr must start at 0 and end at nnz";
+  for (int i = 0; i < n; ++i) {
+    const int32_t b = W.row_ptr[i], e = W.row_ptr[i + 1];
+    if (e < b || b < 0 || e > W.nnz) return format("CSR row_ptr not monotone at row %d", i);
+    double sum = 0.0;
+    for (int32_t k = b; k < e; ++k) {
+      const int32_t c = W.col[k];
+      if (c < 0 || c >= n) return format("CSR column %d out of range in row %d", c, i);
+      if (k > b && c <= W.col[k - 1]) return format("CSR columns not strictly ascending in row %d", i);
+      if (!std::isfinite(W.val[k])) return format("CSR weight not finite in row %d", i);
+      sum += static_cast<double>(W.val[k]);
+    }
+    if (std::fabs(sum - 1.0) > 1e-6) return format("CSR row %d sums to %.9g, not 1", i, sum);
+  }
+  return "";
+}
+
+// Workgroup shape of the gossip kernel: the widest vector (4, 2, 1 columns
+// per thread) whose LDS footprint lets at least four workgroups share a CU;
+// narrower workgroups only when even that does not fit one workgroup.
+gasloc::LaunchShape pick_gossip_shape(const gasloc_ctx& c, int nnz_max) {
+  gasloc::LaunchShape s{4, 256, 0};
+  const size_t budget = c.lds_per_cu / 4;
+  for (int vec : {4, 2, 1}) {
+    s.vec = vec;
+    if (gasloc::gossip_lds_bytes(c.n, nnz_max, s) + gasloc::kStaticLds <= budget) break;
+  }
+  while (s.threads > 64 &&
+         gasloc::gossip_lds_bytes(c.n, nnz_max, s) + gasloc::kStaticLds > c.lds_per_block_max)
+    s.threads /= 2;
+  return s;
+}
+
+int gossip_blocks(const gasloc_ctx& c, const gasloc::LaunchShape& s, int nnz) {
+  const size_t lds = gasloc::gossip_lds_bytes(c.n, nnz, s) + gasloc::kStaticLds;
+  int per_cu = static_cast<int>(std::min<size_t>(c.lds_per_cu / std::max<size_t>(lds, 1), 8));
+  per_cu = std::max(per_cu, 1);
+  const int64_t groups = (c.P + s.vec - 1) / s.vec;
+  const int64_t needed = (groups + s.threads - 1) / s.threads;
+  return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(needed, int64_t(c.cus) * per_cu)));
+}
+
+// Optional shape override for tuning sweeps: GASLOC_GOSSIP_SHAPE="vec,threads,blocks".
+void apply_shape_override(gasloc::LaunchShape* s) {
+  const char* env = std::getenv("GASLOC_GOSSIP_SHAPE");
+  if (!env) return;
+  int v = 0, t = 0, b = 0;
+  if (std::sscanf(env, "%d,%d,%d", &v, &t, &b) == 3 && (v == 1 || v == 2 || v == 4) &&
+      (t == 64 || t == 128 || t == 256) && b >= 0 && b <= kMaxGridBlocks) {
+    s->vec = v;
+    s->threads = t;
+    s->blocks = b;  // 0: keep the computed count
+  }
+}
+
+void release(gasloc_ctx* c) {
+  if (!c) return;
+  (void)hipStreamSynchronize(c->stream);
+  for (int i = 0; i < kStageSlots; ++i) {
+    if (c->stage_done[i]) (void)hipEventDestroy(c->stage_done[i]);
+    if (c->h_stage[i]) (void)hipHostFree(c->h_stage[i]);
+  }
+  if (c->h_ce) (void)hipHostFree(c->h_ce);
+  if (c->d_csr) (void)hipFree(c->d_csr);
+  if (c->d_partials) (void)hipFree(c->d_partials);
+  if (c->d_ce) (void)hipFree(c->d_ce);
+  delete c;
+}
+
+// Copies a CSR into the next pinned slot and enqueues its upload to d_csr.
+gasloc_status upload_csr(gasloc_ctx* c, const int32_t* row_ptr, const int32_t* col, const float* val,
+                         int nnz) {
+  const int slot = c->stage_next;
+  c->stage_next = (c->stage_next + 1) % kStageSlots;
+  if (c->stage_used[slot]) HIP_TRY(c, hipEventSynchronize(c->stage_done[slot]));
+  unsigned char* h = c->h_stage[slot];
+  const size_t rp_bytes = sizeof(int32_t) * static_cast<size_t>(c->n + 1);
+  const size_t nn = static_cast<size_t>(c->n) * c->n;
+  std::memcpy(h, row_ptr, rp_bytes);
+  std::memcpy(h + rp_bytes, col, sizeof(int32_t) * static_cast<size_t>(nnz));
+  std::memcpy(h + rp_bytes + sizeof(int32_t) * nn, val, sizeof(float) * static_cast<size_t>(nnz));
+  HIP_TRY(c, hipMemcpyAsync(c->d_csr, h, csr_stage_bytes(c->n), hipMemcpyHostToDevice, c->stream));
+  HIP_TRY(c, hipEventRecord(c->stage_done[slot], c->stream));
+  c->stage_used[slot] = true;
+  return GASLOC_OK;
+}
+
+gasloc_status reduce_cols(gasloc_ctx* c, int64_t p0, int64_t p1) {
+  HIP_TRY(c, gasloc::launch_consensus_error(c->buf.x, c->hp.param_dtype, c->buf.ld, c->n, p0, p1,
+                                            c->d_partials, c->reduce_blocks, c->stream));
+  HIP_TRY(c, gasloc::launch_finalize(c->d_partials, c->reduce_blocks, c->d_ce, c->stream));
+  return GASLOC_OK;
+}
+
+gasloc_status read_ce(gasloc_ctx* c, double* out) {
+  HIP_TRY(c, hipMemcpyAsync(c->h_ce, c->d_ce, sizeof(double), hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  *out = *c->h_ce;
+  return GASLOC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+gasloc_status gasloc_init(int32_t n, int64_t P, const gasloc_topology* topology,
+                          const gasloc_hparams* hparams, const gasloc_buffers* buffers, void* hip_stream,
+                          gasloc_ctx** out) {
+  if (!out) return fail(nullptr, GASLOC_EINVAL, "out must not be NULL");
+  *out = nullptr;
+  if (!topology || !hparams || !buffers) return fail(nullptr, GASLOC_EINVAL, "NULL argument");
+  if (n < 1 || n > kMaxReplicas) return fail(nullptr, GASLOC_EINVAL, format("n=%d outside [1, 64]", n));
+  if (P < 1 || P >= (int64_t(1) << 31))
+    return fail(nullptr, GASLOC_EINVAL, format("P=%lld outside [1, 2^31)", (long long)P));
+  const std::string hp_err = check_hparams(*hparams);
+  if (!hp_err.empty()) return fail(nullptr, GASLOC_EINVAL, hp_err);
+  const gasloc_buffers& b = *buffers;
+  const size_t sp = param_bytes(hparams->param_dtype);
+  if (b.ld < P) return fail(nullptr, GASLOC_EINVAL, "ld must be >= P");
+  if ((static_cast<uint64_t>(b.ld) * sp) % 16 != 0)
+    return fail(nullptr, GASLOC_EINVAL, "ld * sizeof(param) must be a multiple of 16 bytes");
+  if (!b.x || !b.y || !b.m || !b.v) return fail(nullptr, GASLOC_EINVAL, "x, y, m, v must not be NULL");
+  if (!b.u && hparams->outer_momentum != 0.0f)
+    return fail(nullptr, GASLOC_EINVAL, "u may be NULL only when outer_momentum == 0");
+  if (!b.zp && hparams->consensus_momentum != 0.0f)
+    return fail(nullptr, GASLOC_EINVAL, "zp may be NULL only when consensus_momentum == 0");
+  const void* const all_buffers[] = {b.x, b.y, b.m, b.v, b.u, b.zp};
+  for (const void* p : all_buffers)
+    if (p && !aligned16(p)) return fail(nullptr, GASLOC_EINVAL, "buffers must be 16-byte aligned");
+  if (topology->kind < GASLOC_TOPO_EXPLICIT || topology->kind > GASLOC_TOPO_RANDOM_REGULAR)
+    return fail(nullptr, GASLOC_EINVAL, format("unknown topology kind %d", topology->kind));
+
+  gasloc_ctx* c = new (std::nothrow) gasloc_ctx();
+  if (!c) return fail(nullptr, GASLOC_ENOMEM, "context allocation failed");
+  c->n = n;
+  c->P = P;
+  c->topo = *topology;
+  c->hp = *hparams;
+  c->buf = b;
+  c->stream = static_cast<hipStream_t>(hip_stream);
+  c->k.assign(static_cast<size_t>(n), 0);
+  c->stepped.assign(static_cast<size_t>(n), 0);
+  c->row_ptr.resize(static_cast<size_t>(n) + 1);
+  c->col.resize(static_cast<size_t>(n) * n);
+  c->val.resize(static_cast<size_t>(n) * n);
+
+  if (c->topo.kind != GASLOC_TOPO_EXPLICIT) {
+    int32_t nnz = 0;
+    std::string err;
+    if (!gasloc::make_topology(c->topo, n, 0, c->row_ptr.data(), c->col.data(), c->val.data(), n * n,
+                               &nnz, &err)) {
+      delete c;
+      return fail(nullptr, GASLOC_EINVAL, "topology: " + err);
+    }
+  }
+
+  auto init_fail = [&](hipError_t e, const char* what) {
+    g_thread_error = format("%s: %s", what, hipGetErrorString(e));
+    release(c);
+    return GASLOC_EDEVICE;
+  };
+  hipError_t e = hipGetDevice(&c->device);
+  if (e != hipSuccess) return init_fail(e, "hipGetDevice");
+  hipDeviceProp_t prop;
+  e = hipGetDeviceProperties(&prop, c->device);
+  if (e != hipSuccess) return init_fail(e, "hipGetDeviceProperties");
+  c->cus = std::max(1, prop.multiProcessorCount);
+  c->lds_per_block_max = prop.sharedMemPerBlock;
+  c->lds_per_cu = prop.maxSharedMemoryPerMultiProcessor > 0 ? prop.maxSharedMemoryPerMultiProcessor
+                                                             : prop.sharedMemPerBlock;
+
+  // the densest CSR a round may bring (n*n entries) must still fit one workgroup
+  const gasloc::LaunchShape worst = pick_gossip_shape(*c, n * n);
+  if (gasloc::gossip_lds_bytes(n, n * n, worst) + gasloc::kStaticLds > c->lds_per_block_max) {
+    release(c);
+    return fail(nullptr, GASLOC_EINVAL, "gossip workgroup does not fit the device's LDS");
+  }
+  c->adam_blocks_total = c->cus * 8;
+  c->reduce_blocks = std::min(kMaxGridBlocks, c->cus * 4);
+  c->partial_cap = kMaxGridBlocks;
+
+  if ((e = hipMalloc(&c->d_csr, csr_stage_bytes(n))) != hipSuccess) return init_fail(e, "hipMalloc csr");
+  if ((e = hipMalloc(&c->d_partials, sizeof(double) * c->partial_cap)) != hipSuccess)
+    return init_fail(e, "hipMalloc partials");
+  if ((e = hipMalloc(&c->d_ce, sizeof(double))) != hipSuccess) return init_fail(e, "hipMalloc ce");
+  if ((e = hipHostMalloc(&c->h_ce, sizeof(double), hipHostMallocDefault)) != hipSuccess)
+    return init_fail(e, "hipHostMalloc ce");
+  for (int i = 0; i < kStageSlots; ++i) {
+    if ((e = hipHostMalloc(&c->h_stage[i], csr_stage_bytes(n), hipHostMallocDefault)) != hipSuccess)
+      return init_fail(e, "hipHostMalloc staging");
+    if ((e = hipEventCreateWithFlags(&c->stage_done[i], hipEventDisableTiming)) != hipSuccess)
+      return init_fail(e, "hipEventCreate");
+  }
+
+  // zero the optimizer state of every worker: m, v, u, zp
+  const size_t state_bytes = sizeof(float) * static_cast<size_t>(n) * static_cast<size_t>(b.ld);
+  for (float* p : {b.m, b.v, b.u, b.zp}) {
+    if (!p) continue;
+    if ((e = hipMemsetAsync(p, 0, state_bytes, c->stream)) != hipSuccess) return init_fail(e, "hipMemsetAsync");
+  }
+  *out = c;
+  return GASLOC_OK;
+}
+
+gasloc_status gasloc_local_step(gasloc_ctx* c, const float* grads, int64_t grad_ld, const uint8_t* active,
+                                float lr) {
+  if (!c) return fail(nullptr, GASLOC_EINVAL, "NULL context");
+  if (c->failed) return fail(c, GASLOC_ESTATE, "context unusable after a device error: " + c->err);
+  if (!grads || !aligned16(grads)) return fail(c, GASLOC_EINVAL, "grads must be non-NULL and 16-byte aligned");
+  if (grad_ld < c->P || (grad_ld * 4) % 16 != 0)
+    return fail(c, GASLOC_EINVAL, "grad_ld must be >= P and a multiple of 4");
+  if (!(std::isfinite(lr) && lr >= 0.0f)) return fail(c, GASLOC_EINVAL, "lr must be finite and >= 0");
+  DeviceGuard guard(c->device);
+
+  gasloc::AdamArgs a{};
+  a.x = c->buf.x;
+  a.y = c->buf.y;
+  a.m = c->buf.m;
+  a.v = c->buf.v;
+  a.g = grads;
+  a.ld = c->buf.ld;
+  a.gld = grad_ld;
+  a.P = c->P;
+  const double lr64 = lr, b1 = c->hp.beta1, b2 = c->hp.beta2;
+  a.c_wd = static_cast<float>(1.0 - lr64 * static_cast<double>(c->hp.weight_decay));
+  a.b1 = c->hp.beta1;
+  a.b2 = c->hp.beta2;
+  a.omb1 = static_cast<float>(1.0 - b1);
+  a.omb2 = static_cast<float>(1.0 - b2);
+  a.eps = c->hp.eps;
+  int slots = 0;
+  for (int i = 0; i < c->n; ++i) {
+    if (active && !active[i]) continue;
+    const int64_t k = c->k[static_cast<size_t>(i)] + 1;
+    a.rep[slots] = i;
+    a.s1[slots] = static_cast<float>(lr64 / (1.0 - std::pow(b1, static_cast<double>(k))));
+    a.c2[slots] = static_cast<float>(std::sqrt(1.0 - std::pow(b2, static_cast<double>(k))));
+    if (!c->stepped[static_cast<size_t>(i)]) a.from_x |= (1ull << slots);
+    ++slots;
+  }
+  if (slots == 0) return GASLOC_OK;
+  a.n_active = slots;
+  const int64_t groups = (c->P + 3) / 4;
+  const int64_t want = std::max<int64_t>(1, c->adam_blocks_total / slots);
+  const int per_worker = static_cast<int>(std::min<int64_t>(want, (groups + 255) / 256));
+  HIP_TRY(c, gasloc::launch_local_adamw(a, c->hp.param_dtype, per_worker, c->stream));
+  for (int s = 0; s < slots; ++s) {
+    c->k[static_cast<size_t>(a.rep[s])] += 1;
+    c->stepped[static_cast<size_t>(a.rep[s])] = 1;
+  }
+  return GASLOC_OK;
+}
+
+gasloc_status gasloc_gossip_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t) {
+  if (!c) return fail(nullptr, GASLOC_EINVAL, "NULL context");
+  if (c->failed) return fail(c, GASLOC_ESTATE, "context unusable after a device error: " + c->err);
+  const int32_t *rp, *col;
+  const float* val;
+  int32_t nnz = 0;
+  if (W) {
+    const std::string e = check_csr(*W, c->n);
+    if (!e.empty()) return fail(c, GASLOC_EINVAL, e);
+    rp = W->row_ptr;
+    col = W->col;
+    val = W->val;
+    nnz = W->nnz;
+  } else {
+    if (c->topo.kind == GASLOC_TOPO_EXPLICIT)
+      return fail(c, GASLOC_EINVAL, "EXPLICIT topology: pass W to every round");
+    std::string err;
+    if (!gasloc::make_topology(c->topo, c->n, t, c->row_ptr.data(), c->col.data(), c->val.data(),
+                               c->n * c->n, &nnz, &err))
+      return fail(c, GASLOC_EINVAL, "topology: " + err);
+    rp = c->row_ptr.data();
+    col = c->col.data();
+    val = c->val.data();
+  }
+  DeviceGuard guard(c->device);
+  gasloc_status st = upload_csr(c, rp, col, val, nnz);
+  if (st != GASLOC_OK) return st;
+
+  gasloc::GossipArgs a{};
+  a.x = c->buf.x;
+  a.y = c->buf.y;
+  a.u = c->buf.u;
+  a.zp = c->buf.zp;
+  const size_t rp_bytes = sizeof(int32_t) * static_cast<size_t>(c->n + 1);
+  a.row_ptr = reinterpret_cast<const int32_t*>(c->d_csr);
+  a.col = reinterpret_cast<const int32_t*>(c->d_csr + rp_bytes);
+  a.val = reinterpret_cast<const float*>(c->d_csr + rp_bytes + sizeof(int32_t) * c->n * c->n);
+  a.ld = c->buf.ld;
+  a.P = c->P;
+  a.n = c->n;
+  a.nnz = nnz;
+  a.mu = c->hp.outer_momentum;
+  a.eta = c->hp.outer_lr;
+  a.gamma = c->hp.consensus_momentum;
+  a.nesterov = c->hp.outer_nesterov;
+  a.use_u = c->buf.u != nullptr;
+  a.store_zp = c->hp.consensus_momentum != 0.0f;
+  a.apply_gamma = a.store_zp && c->rounds_done > 0;
+  for (int i = 0; i < c->n; ++i)
+    if (c->stepped[static_cast<size_t>(i)]) a.stepped |= (1ull << i);
+
+  gasloc::LaunchShape shape = pick_gossip_shape(*c, nnz);
+  shape.blocks = gossip_blocks(*c, shape, nnz);
+  apply_shape_override(&shape);
+  if (shape.blocks == 0) shape.blocks = gossip_blocks(*c, shape, nnz);
+  shape.blocks = std::min(shape.blocks, c->partial_cap);
+  if (gasloc::gossip_lds_bytes(c->n, nnz, shape) + gasloc::kStaticLds > c->lds_per_block_max)
+    return fail(c, GASLOC_EINVAL, "gossip shape exceeds the device's LDS per workgroup");
+  a.partials = c->d_partials;
+  HIP_TRY(c, gasloc::launch_gossip_round(a, c->hp.param_dtype, shape, c->stream));
+  HIP_TRY(c, gasloc::launch_finalize(c->d_partials, shape.blocks, c->d_ce, c->stream));
+  c->rounds_done += 1;
+  std::fill(c->stepped.begin(), c->stepped.end(), 0);
+  c->ce_current = true;
+  return GASLOC_OK;
+}
+
+gasloc_status gasloc_consensus_error(gasloc_ctx* c, double* out) {
+  if (!c || !out) return fail(c, GASLOC_EINVAL, "NULL argument");
+  if (c->failed) return fail(c, GASLOC_ESTATE, "context unusable after a device error: " + c->err);
+  DeviceGuard guard(c->device);
+  if (!c->ce_current) {
+    gasloc_status st = reduce_cols(c, 0, c->P);
+    if (st != GASLOC_OK) return st;
+    c->ce_current = true;
+  }
+  return read_ce(c, out);
+}
+
+gasloc_status gasloc_consensus_error_cols(gasloc_ctx* c, int64_t p_begin, int64_t p_end, double* out) {
+  if (!c || !out) return fail(c, GASLOC_EINVAL, "NULL argument");
+  if (c->failed) return fail(c, GASLOC_ESTATE, "context unusable after a device error: " + c->err);
+  if (p_begin < 0 || p_end < p_begin || p_end > c->P)
+    return fail(c, GASLOC_EINVAL, "need 0 <= p_begin <= p_end <= P");
+  DeviceGuard guard(c->device);
+  gasloc_status st = reduce_cols(c, p_begin, p_end);
+  if (st != GASLOC_OK) return st;
+  c->ce_current = false;  // d_ce now holds a partial sum
+  return read_ce(c, out);
+}
+
+gasloc_status gasloc_replica_mean(gasloc_ctx* c, void* out) {
+  if (!c) return fail(nullptr, GASLOC_EINVAL, "NULL context");
+  if (c->failed) return fail(c, GASLOC_ESTATE, "context unusable after a device error: " + c->err);
+  if (!out || !aligned16(out)) return fail(c, GASLOC_EINVAL, "out must be non-NULL and 16-byte aligned");
+  DeviceGuard guard(c->device);
+  HIP_TRY(c, gasloc::launch_replica_mean(c->buf.x, c->hp.param_dtype, c->buf.ld, c->n, c->P, out,
+                                         c->reduce_blocks, c->stream));
+  return GASLOC_OK;
+}
+
+gasloc_status gasloc_topology_csr(gasloc_ctx* c, uint64_t t, int32_t* row_ptr, int32_t* col, float* val,
+                                  int32_t cap, int32_t* nnz) {
+  if (!c) return fail(nullptr, GASLOC_EINVAL, "NULL context");
+  if (!row_ptr || !col || !val || !nnz) return fail(c, GASLOC_EINVAL, "NULL output array");
+  if (c->topo.kind == GASLOC_TOPO_EXPLICIT) return fail(c, GASLOC_EINVAL, "EXPLICIT topology has no generator");
+  std::string err;
+  if (!gasloc::make_topology(c->topo, c->n, t, row_ptr, col, val, cap, nnz, &err))
+    return fail(c, GASLOC_EINVAL, "topology: " + err);
+  return GASLOC_OK;
+}
+
+gasloc_status gasloc_make_topology(const gasloc_topology* topology, int32_t n, uint64_t t, int32_t* row_ptr,
+                                   int32_t* col, float* val, int32_t cap, int32_t* nnz) {
+  if (!topology || !row_ptr || !col || !val || !nnz) return fail(nullptr, GASLOC_EINVAL, "NULL argument");
+  std::string err;
+  if (!gasloc::make_topology(*topology, n, t, row_ptr, col, val, cap, nnz, &err))
+    return fail(nullptr, GASLOC_EINVAL, "topology: " + err);
+  return GASLOC_OK;
+}
+
+gasloc_status gasloc_validate_csr(const gasloc_csr* W, int32_t n) {
+  if (!W) return fail(nullptr, GASLOC_EINVAL, "NULL CSR");
+  if (n < 1 || n > kMaxReplicas) return fail(nullptr, GASLOC_EINVAL, "n outside [1, 64]");
+  const std::string e = check_csr(*W, n);
+  if (!e.empty()) return fail(nullptr, GASLOC_EINVAL, e);
+  return GASLOC_OK;
+}
+
+gasloc_status gasloc_get_counters(const gasloc_ctx* c, int64_t* k, uint8_t* stepped, int64_t* rounds_done) {
+  if (!c) return fail(nullptr, GASLOC_EINVAL, "NULL context");
+  for (int i = 0; i < c->n; ++i) {
+    if (k) k[i] = c->k[static_cast<size_t>(i)];
+    if (stepped) stepped[i] = c->stepped[static_cast<size_t>(i)];
+  }
+  if (rounds_done) *rounds_done = c->rounds_done;
+  return GASLOC_OK;
+}
+
+gasloc_status gasloc_set_counters(gasloc_ctx* c, const int64_t* k, const uint8_t* stepped, int64_t rounds_done) {
+  if (!c) return fail(nullptr, GASLOC_EINVAL, "NULL context");
+  if (rounds_done < 0) return fail(c, GASLOC_EINVAL, "rounds_done must be >= 0");
+  if (k)
+    for (int i = 0; i < c->n; ++i)
+      if (k[i] < 0) return fail(c, GASLOC_EINVAL, "step counts must be >= 0");
+  for (int i = 0; i < c->n; ++i) {
+    if (k) c->k[static_cast<size_t>(i)] = k[i];
+    if (stepped) c->stepped[static_cast<size_t>(i)] = stepped[i] ? 1 : 0;
+  }
+  c->rounds_done = rounds_done;
+  c->ce_current = false;
+  return GASLOC_OK;
+}
+
+const char* gasloc_last_error(const gasloc_ctx* c) { return c ? c->err.c_str() : g_thread_error.c_str(); }
+
+void gasloc_destroy(gasloc_ctx* c) {
+  if (!c) return;
+  DeviceGuard guard(c->device);
+  release(c);
+}
+
+}  // extern "C"

@@ -1,0 +1,185 @@
+"""Host-side tests of libgasloc.so (no GPU): exported symbols, bit-exact
+round schedules against the oracle, CSR validation and argument checks that
+fail before any device call."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2606_11081_amd as g
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+KINDS = ["ring", "complete", "exponential", "one_peer_exp", "one_peer", "two_peer", "random_regular"]
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "gasloc.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gasloc_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    lib = g.library()
+    names = header_functions()
+    assert len(names) >= 13
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(names) == set(g.gasloc._SIGNATURES)
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("n", [1, 2, 3, 4, 5, 7, 8, 16, 32, 33, 64])
+def test_schedule_bit_exact_with_oracle(kind, n):
+    if kind == "random_regular" and (n <= 3 or (3 * n) % 2):
+        pytest.skip("3-regular graph needs n > 3 and 3n even")
+    topo = g.make_topology_struct(kind, seed=3, degree=3)
+    rounds = 200 if n <= 16 else 40
+    for t in range(rounds):
+        rp, col, val = g.gasloc_make_topology(topo, n, t)
+        orp, ocol, oval = oracle.topology_csr(kind, n, 3, t, 3)
+        assert np.array_equal(rp, orp), (kind, n, t)
+        assert np.array_equal(col, ocol), (kind, n, t)
+        assert np.array_equal(val.view(np.uint32), oval.view(np.uint32)), (kind, n, t)
+
+
+@pytest.mark.parametrize("kind,n,degree", [("random_regular", 10, 4), ("random_regular", 12, 5),
+                                           ("random_regular", 9, 0), ("two_peer", 64, 3)])
+def test_schedule_bit_exact_other_degrees_and_seeds(kind, n, degree):
+    for seed in (0, 1, 2 ** 63 + 5):
+        topo = g.make_topology_struct(kind, seed=seed, degree=degree)
+        for t in (0, 1, 17, 2 ** 40 + 3):
+            got = g.gasloc_make_topology(topo, n, t)
+            exp = oracle.topology_csr(kind, n, seed, t, degree)
+            for a, b in zip(got, exp):
+                assert np.array_equal(a, b)
+
+
+def test_schedule_long_horizon_matching_n64():
+    topo = g.make_topology_struct("one_peer", seed=3)
+    for t in range(0, 1000, 7):
+        got = g.gasloc_make_topology(topo, 64, t)
+        exp = oracle.topology_csr("one_peer", 64, 3, t)
+        for a, b in zip(got, exp):
+            assert np.array_equal(a, b)
+
+
+def test_make_topology_rejects_bad_arguments():
+    with pytest.raises(g.GaslocError, match="EINVAL"):
+        g.gasloc_make_topology(g.make_topology_struct("random_regular", degree=3), 5, 0)  # 3*5 odd
+    with pytest.raises(g.GaslocError, match="EINVAL"):
+        g.gasloc_make_topology(g.make_topology_struct("random_regular", degree=4), 4, 0)  # degree >= n
+    with pytest.raises(g.GaslocError, match="EINVAL"):
+        g.gasloc_make_topology(g.make_topology_struct(99), 4, 0)
+    with pytest.raises(g.GaslocError, match="EINVAL"):
+        g.gasloc_make_topology(g.make_topology_struct("explicit"), 4, 0)
+    with pytest.raises(g.GaslocError, match="EINVAL"):
+        g.gasloc_make_topology(g.make_topology_struct("ring"), 65, 0)
+    # capacity too small
+    lib = g.library()
+    rp = np.zeros(9, np.int32)
+    col = np.zeros(4, np.int32)
+    val = np.zeros(4, np.float32)
+    nnz = ctypes.c_int32()
+    topo = g.make_topology_struct("complete")
+    st = lib.gasloc_make_topology(ctypes.byref(topo), 8, 0, rp.ctypes.data, col.ctypes.data,
+                                  val.ctypes.data, 4, ctypes.byref(nnz))
+    assert st == g.GASLOC_EINVAL
+    assert "capacity" in g.gasloc_last_error()
+
+
+def _ring4():
+    return oracle.topology_csr("ring", 4, 0, 0)
+
+
+def test_validate_csr_accepts_generated_graphs():
+    for kind in KINDS:
+        n = 8
+        W = oracle.topology_csr(kind, n, 3, 5, 3)
+        g.gasloc_validate_csr(W, n)
+
+
+@pytest.mark.parametrize("case", ["n_mismatch", "unsorted", "duplicate", "out_of_range", "negative_col",
+                                  "row_sum", "nan", "rowptr_start", "rowptr_nonmono", "rowptr_end"])
+def test_validate_csr_rejects(case):
+    rp, col, val = (a.copy() for a in _ring4())
+    n = 4
+    if case == "n_mismatch":
+        n = 5
+    elif case == "unsorted":
+        col[0], col[1] = col[1], col[0]
+    elif case == "duplicate":
+        col[1] = col[0]
+    elif case == "out_of_range":
+        col[2] = 4
+    elif case == "negative_col":
+        col[0] = -1
+    elif case == "row_sum":
+        val[0] = 0.5
+    elif case == "nan":
+        val[3] = np.nan
+    elif case == "rowptr_start":
+        rp[0] = 1
+    elif case == "rowptr_nonmono":
+        rp[2] = rp[1] - 1
+    elif case == "rowptr_end":
+        rp[-1] -= 1
+    with pytest.raises(g.GaslocError, match="EINVAL"):
+        g.gasloc_validate_csr((rp, col, val), n)
+
+
+def test_row_sum_tolerance_is_1e6_in_fp64():
+    rp = np.array([0, 1], np.int32)
+    col = np.array([0], np.int32)
+    g.gasloc_validate_csr((rp, col, np.array([1.0 + 9e-7], np.float32)), 1)
+    with pytest.raises(g.GaslocError):
+        g.gasloc_validate_csr((rp, col, np.array([1.0 + 2e-6], np.float32)), 1)
+
+
+# --- gasloc_init argument checks that fail before any HIP call -------------
+
+FAKE = 1 << 20  # a 16-byte aligned address that is never dereferenced
+
+
+def _init(n=4, P=1024, ld=None, hp=None, topo=None, x=FAKE, y=FAKE, m=FAKE, v=FAKE, u=FAKE, zp=FAKE):
+    hp = hp or g.make_hparams()
+    topo = topo or g.make_topology_struct("ring")
+    return g.gasloc_init(n, P, topo, hp, x, y, m, v, u, zp, ld if ld is not None else P)
+
+
+@pytest.mark.parametrize("kwargs,msg", [
+    (dict(n=0), "n=0"),
+    (dict(n=65), "n=65"),
+    (dict(P=0), "P=0"),
+    (dict(P=2 ** 31), "P="),
+    (dict(P=1024, ld=1000), "ld must be"),
+    (dict(P=1023, ld=1023), "multiple of 16"),
+    (dict(x=None), "must not be NULL"),
+    (dict(m=FAKE + 4), "16-byte aligned"),
+    (dict(u=None), "u may be NULL"),
+    (dict(zp=None), "zp may be NULL"),
+    (dict(hp=g.make_hparams(beta1=1.0)), "beta1"),
+    (dict(hp=g.make_hparams(beta2=-0.1)), "beta2"),
+    (dict(hp=g.make_hparams(eps=0.0)), "eps"),
+    (dict(hp=g.make_hparams(outer_lr=0.0)), "outer_lr"),
+    (dict(hp=g.make_hparams(outer_momentum=1.0)), "outer_momentum"),
+    (dict(hp=g.make_hparams(consensus_momentum=1.5)), "consensus_momentum"),
+    (dict(hp=g.make_hparams(weight_decay=float("nan"))), "weight_decay"),
+    (dict(topo=g.make_topology_struct(42)), "topology kind"),
+    (dict(n=5, topo=g.make_topology_struct("random_regular", degree=3)), "topology"),
+])
+def test_init_rejects_bad_arguments(kwargs, msg):
+    with pytest.raises(g.GaslocError, match="EINVAL") as ei:
+        _init(**kwargs)
+    assert msg in str(ei.value)
+
+
+def test_null_context_is_rejected():
+    lib = g.library()
+    assert lib.gasloc_local_step(None, FAKE, 4, None, 0.1) == g.GASLOC_EINVAL
+    assert lib.gasloc_gossip_round(None, None, 0) == g.GASLOC_EINVAL
+    out = ctypes.c_double()
+    assert lib.gasloc_consensus_error(None, ctypes.byref(out)) == g.GASLOC_EINVAL
+    lib.gasloc_destroy(None)  # ignored

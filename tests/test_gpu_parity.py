@@ -1,0 +1,290 @@
+"""GPU parity: the HIP library against the oracle on identical seeded inputs.
+
+Every test calls the library through its C ABI (ctypes binding) on cuda:0.
+"""
+import numpy as np
+import pytest
+
+import gasloc_inputs as gi
+import oracle
+from tests.gpu_harness import Pair, log, reduction_close, within
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2606_11081_amd as g
+
+    g.library()  # fail loudly if the HIP library is missing
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def _run(pair, rounds, H_i, check_every_round=True, tag=""):
+    H_i = np.asarray(H_i)
+    n = pair.n
+    for t in range(rounds):
+        for h in range(int(H_i.max()) if H_i.size else 0):
+            pair.local_step(active=(H_i > h).astype(np.uint8))
+        stepped = np.nonzero(H_i > 0)[0]
+        if t == rounds - 1:
+            pair.check_state(names=("m", "v"), y_rows=stepped, tag="%s round %d pre-gossip" % (tag, t))
+        pair.gossip_round(t)
+        if check_every_round or t == rounds - 1:
+            ce = pair.gpu.consensus_error()
+            o32 = pair.oracles["f32"]
+            ce_ref = o32.consensus_error()
+            reduction_close(ce, ce_ref, "%s round %d consensus error" % (tag, t))
+            if "f64" in pair.oracles:
+                ce64 = pair.oracles["f64"].consensus_error()
+                assert abs(ce - ce64) <= 1e-3 * abs(ce64) + 1e-30, (ce, ce64)
+    assert n == pair.n
+    return pair.check_state(tag=tag)
+
+
+def test_ring_n4_p1m_full_state_ten_rounds():
+    w = gi.WORKLOADS["ring-n4-p1m"]
+    log("case %s: n=%d P=%d" % (w.name, w.n, w.P))
+    pair = Pair(w.n, w.P, w.topology, w.param_dtype, gamma=w.gamma)
+    stats = _run(pair, w.rounds, gi.local_steps(w), tag=w.name)
+    log("bit-exact fraction vs fp32 oracle: %s" % stats)
+    # the kernels follow the oracle's op order: identical bits are expected
+    assert min(stats.values()) == 1.0
+    # network average (Algorithm 1 output)
+    import torch
+
+    out = torch.empty(w.P, dtype=torch.float32, device="cuda")
+    pair.gpu.replica_mean(out)
+    torch.cuda.synchronize()
+    ref = pair.oracles["f32"].replica_mean()
+    assert np.array_equal(out.cpu().numpy().view(np.uint32), ref.view(np.uint32))
+
+
+SMALL = [
+    # n, P, topology, dtype, H, gamma, mu, nesterov
+    (1, 1000, "ring", "f32", 2, 0.1, 0.9, True),
+    (2, 4099, "ring", "f32", 1, 0.1, 0.9, True),
+    (3, 777, "two_peer", "f32", 2, 0.2, 0.9, True),
+    (5, 4097, "one_peer", "f32", 3, 0.0, 0.9, True),
+    (8, 10007, "exponential", "f32", 1, 0.1, 0.9, False),
+    (16, 8191, "one_peer_exp", "f32", 2, 0.1, 0.0, False),
+    (32, 3001, "random_regular", "bf16", 2, 0.1, 0.9, True),
+    (33, 515, "two_peer", "f32", 1, 0.3, 0.5, True),
+    (64, 2053, "complete", "f32", 1, 0.0, 0.9, True),
+    (64, 4099, "one_peer", "bf16", 2, 0.0, 0.9, True),
+    (7, 3, "ring", "f32", 1, 0.1, 0.9, True),
+    (4, 1, "complete", "bf16", 1, 0.1, 0.9, True),
+]
+
+
+@pytest.mark.parametrize("n,P,topology,dtype,H,gamma,mu,nesterov", SMALL)
+def test_small_cases(n, P, topology, dtype, H, gamma, mu, nesterov):
+    log("case n=%d P=%d %s %s H=%d gamma=%g mu=%g nesterov=%s" % (n, P, topology, dtype, H, gamma, mu,
+                                                                   nesterov))
+    pair = Pair(n, P, topology, dtype, gamma=gamma, mu=mu, nesterov=nesterov)
+    H_i = np.full(n, H)
+    if n >= 5:
+        H_i[1] = 0  # a worker that skips its local steps this round (H_i = 0)
+        H_i[-1] = max(1, H - 1)
+    stats = _run(pair, 3, H_i, tag="small")
+    log("bit-exact fraction vs fp32 oracle: %s" % stats)
+    if topology == "complete" and gamma == 0.0:
+        x = pair.gather("x")
+        assert np.all(x == x[0]), "complete graph keeps replicas bit-identical"
+        assert pair.gpu.consensus_error() == 0.0
+
+
+def test_explicit_nonsymmetric_csr_and_identity():
+    n, P = 6, 5003
+    rng = np.random.default_rng(3)
+    pair = Pair(n, P, "ring", "f32", gamma=0.2)
+    for t in range(3):
+        pair.local_step()
+        dense = rng.random((n, n)) * (rng.random((n, n)) < 0.5) + np.eye(n)
+        dense /= dense.sum(axis=1, keepdims=True)
+        rp = np.zeros(n + 1, np.int32)
+        cols, vals = [], []
+        for i in range(n):
+            nz = np.nonzero(dense[i])[0]
+            cols += nz.tolist()
+            vals += dense[i, nz].tolist()
+            rp[i + 1] = len(cols)
+        val = np.array(vals, np.float32)
+        # renormalise in fp32 so each row sums to 1 within the validator's 1e-6
+        W = (rp, np.array(cols, np.int32), val)
+        pair.gossip_round(t, W=W)
+        reduction_close(pair.gpu.consensus_error(), pair.oracles["f32"].consensus_error(), "explicit CE")
+    pair.check_state(tag="explicit")
+
+
+def test_all_inactive_step_changes_nothing():
+    import torch
+
+    n, P = 4, 1024
+    pair = Pair(n, P, "ring", "f32")
+    before = {k: getattr(pair.gpu, k).clone() for k in ("x", "m", "v")}
+    pair.local_step(active=np.zeros(n, np.uint8))
+    torch.cuda.synchronize()
+    for k, t in before.items():
+        assert torch.equal(t, getattr(pair.gpu, k))
+    k, stepped, rounds = pair.gpu.counters()
+    assert list(k) == [0] * n and list(stepped) == [0] * n and rounds == 0
+
+
+def test_runs_are_bit_identical():
+    import torch
+
+    outs = []
+    for _ in range(2):
+        pair = Pair(16, 100_003, "one_peer_exp", "f32", precisions=("f32",))
+        for t in range(2):
+            pair.local_step()
+            pair.local_step()
+            pair.gossip_round(t)
+        ce = pair.gpu.consensus_error()
+        torch.cuda.synchronize()
+        outs.append((pair.gpu.x.clone(), pair.gpu.u.clone(), pair.gpu.zp.clone(), ce))
+    for a, b in zip(outs[0][:3], outs[1][:3]):
+        assert torch.equal(a, b)
+    assert outs[0][3] == outs[1][3]
+
+
+def test_checkpoint_resume_is_bit_exact():
+    import torch
+
+    import paper_2606_11081_amd as g
+
+    n, P = 8, 20_001
+    full = Pair(n, P, "two_peer", "f32", precisions=("f32",))
+    for t in range(2):
+        full.local_step()
+        full.gossip_round(t)
+    torch.cuda.synchronize()
+    saved = {k: getattr(full.gpu, k).clone() for k in ("x", "y", "m", "v", "u", "zp")}
+    k, stepped, rounds = full.gpu.counters()
+    step = full.step
+    for t in range(2, 4):
+        full.local_step()
+        full.gossip_round(t)
+    torch.cuda.synchronize()
+
+    resumed = Pair(n, P, "two_peer", "f32", precisions=("f32",))
+    torch.cuda.synchronize()
+    for name, t_ in saved.items():
+        getattr(resumed.gpu, name).copy_(t_)
+    g.gasloc_set_counters(resumed.gpu.ctx, k, stepped, rounds)
+    resumed.step = step
+    for t in range(2, 4):
+        resumed.local_step()
+        resumed.gossip_round(t)
+    torch.cuda.synchronize()
+    for name in ("x", "m", "v", "u", "zp"):
+        assert torch.equal(getattr(full.gpu, name), getattr(resumed.gpu, name)), name
+    assert full.gpu.consensus_error() == resumed.gpu.consensus_error()
+
+
+def test_consensus_error_columns_and_closed_form():
+    import torch
+
+    n, P = 16, 1_000_003
+    pair = Pair(n, P, "one_peer_exp", "f32", precisions=("f32",))
+    pair.local_step()
+    pair.gossip_round(0)
+    fused = pair.gpu.consensus_error()
+    total = pair.gpu.consensus_error_cols(0, P)
+    reduction_close(total, fused, "standalone vs fused")
+    o = pair.oracles["f32"]
+    for a, b in [(0, 1), (0, 4097), (5, 70_001), (P - 999, P), (123_456, 123_456)]:
+        got = pair.gpu.consensus_error_cols(a, b)
+        reduction_close(got, o.consensus_error(slice(a, b)) if b > a else 0.0, "cols [%d,%d)" % (a, b))
+    # closed form: x_i = c_i on every column -> CE = P * sum_i (c_i - cbar)^2 exactly
+    c = torch.arange(1, n + 1, dtype=torch.float32, device="cuda").view(n, 1)
+    pair.gpu.x[:, :P].copy_(c.expand(n, P))
+    expect = P * float(((np.arange(1, n + 1) - (n + 1) / 2.0) ** 2).sum())
+    assert pair.gpu.consensus_error_cols(0, P) == expect
+
+
+def test_error_paths_on_device():
+    import torch
+
+    import paper_2606_11081_amd as g
+
+    pair = Pair(4, 1024, "ring", "f32", precisions=("f32",))
+    ctx = pair.gpu.ctx
+    with pytest.raises(g.GaslocError, match="EINVAL"):
+        g.gasloc_local_step(ctx, pair.grads.data_ptr() + 4, pair.gpu.ld, None, 0.1)  # misaligned
+    with pytest.raises(g.GaslocError, match="EINVAL"):
+        g.gasloc_local_step(ctx, pair.grads, pair.gpu.ld, None, float("nan"))
+    bad = (np.array([0, 1, 2, 3, 4], np.int32), np.array([0, 1, 2, 4], np.int32),
+           np.ones(4, np.float32))
+    with pytest.raises(g.GaslocError, match="out of range"):
+        g.gasloc_gossip_round(ctx, bad, 0)
+    with pytest.raises(g.GaslocError, match="EINVAL"):
+        g.gasloc_consensus_error_cols(ctx, 5, 4)
+    # the context keeps working after argument errors
+    pair.local_step()
+    pair.gossip_round(0)
+    reduction_close(pair.gpu.consensus_error(), pair.oracles["f32"].consensus_error(), "after errors")
+    # explicit topology needs W every round
+    gexp = g.GASLoC(4, 256, topology="explicit")
+    with pytest.raises(g.GaslocError, match="EXPLICIT"):
+        g.gasloc_gossip_round(gexp.ctx, None, 0)
+    torch.cuda.synchronize()
+
+
+def test_topology_csr_from_context_matches_oracle():
+    import paper_2606_11081_amd as g
+
+    gpu = g.GASLoC(32, 256, topology="random_regular", seed=3, degree=3)
+    for t in range(20):
+        got = g.gasloc_topology_csr(gpu.ctx, t, 32)
+        exp = oracle.topology_csr("random_regular", 32, 3, t, 3)
+        for a, b in zip(got, exp):
+            assert np.array_equal(a, b)
+
+
+# ---------------------------------------------------------------------------
+# full-size workloads: sampled columns (first/last 64 plus uniform picks)
+# ---------------------------------------------------------------------------
+
+FULL = [
+    ("exp-n8-p124m", 1 << 18, 4),
+    ("onepeer-exp-n16-p350m", 1 << 17, 3),
+    ("regular3-n32-p150m-bf16", 1 << 15, 2),
+    ("matching-n64-p50m-hetH", 1 << 14, 2),
+]
+
+
+@pytest.mark.parametrize("name,sample,rounds", FULL)
+def test_full_size_sampled(name, sample, rounds):
+    import torch
+
+    w = gi.WORKLOADS[name]
+    log("case %s (sampled %d columns, %d rounds)" % (name, sample, rounds))
+    cols = gi.sample_columns(w.P, sample)
+    pair = Pair(w.n, w.P, w.topology, w.param_dtype, gamma=w.gamma, degree=w.degree, cols=cols,
+                precisions=("f32",) if w.param_dtype == "bf16" else ("f32", "f64"))
+    H_i = gi.local_steps(w)
+    H_i = np.minimum(H_i, 12)  # keep the oracle's share short; the kernels see the same masks
+    for t in range(rounds):
+        for h in range(int(H_i.max())):
+            pair.local_step(active=(H_i > h).astype(np.uint8))
+        pair.gossip_round(t)
+        fused = pair.gpu.consensus_error()
+        assert np.isfinite(fused) and fused >= 0.0
+        # edge slices of the row are contiguous in both index spaces
+        head = pair.gpu.consensus_error_cols(0, 64)
+        tail = pair.gpu.consensus_error_cols(w.P - 64, w.P)
+        o = pair.oracles["f32"]
+        reduction_close(head, o.consensus_error(slice(0, 64)), "%s round %d CE head" % (name, t))
+        reduction_close(tail, o.consensus_error(slice(len(cols) - 64, len(cols))), "%s CE tail" % name)
+        log("round %d: CE %.6e" % (t, fused))
+    stats = pair.check_state(tag=name)
+    log("bit-exact fraction vs fp32 oracle: %s" % stats)
+    del pair
+    torch.cuda.empty_cache()
