@@ -41,8 +41,10 @@ def _run(pair, rounds, H_i, check_every_round=True, tag=""):
             ce_ref = o32.consensus_error()
             reduction_close(ce, ce_ref, "%s round %d consensus error" % (tag, t))
             if "f64" in pair.oracles:
+                # fp64-state drift check (loose); identical replicas give fp64
+                # rounding residue of order 1e-30 per element in the fp64 oracle
                 ce64 = pair.oracles["f64"].consensus_error()
-                assert abs(ce - ce64) <= 1e-3 * abs(ce64) + 1e-30, (ce, ce64)
+                assert abs(ce - ce64) <= 1e-3 * abs(ce64) + 1e-24 * n * pair.P, (ce, ce64)
     assert n == pair.n
     return pair.check_state(tag=tag)
 
@@ -148,7 +150,8 @@ def test_runs_are_bit_identical():
             pair.gossip_round(t)
         ce = pair.gpu.consensus_error()
         torch.cuda.synchronize()
-        outs.append((pair.gpu.x.clone(), pair.gpu.u.clone(), pair.gpu.zp.clone(), ce))
+        P = pair.P  # columns beyond P (row padding) are never touched by the library
+        outs.append((pair.gpu.x[:, :P].clone(), pair.gpu.u[:, :P].clone(), pair.gpu.zp[:, :P].clone(), ce))
     for a, b in zip(outs[0][:3], outs[1][:3]):
         assert torch.equal(a, b)
     assert outs[0][3] == outs[1][3]
@@ -184,7 +187,7 @@ def test_checkpoint_resume_is_bit_exact():
         resumed.gossip_round(t)
     torch.cuda.synchronize()
     for name in ("x", "m", "v", "u", "zp"):
-        assert torch.equal(getattr(full.gpu, name), getattr(resumed.gpu, name)), name
+        assert torch.equal(getattr(full.gpu, name)[:, :P], getattr(resumed.gpu, name)[:, :P]), name
     assert full.gpu.consensus_error() == resumed.gpu.consensus_error()
 
 
