@@ -63,6 +63,7 @@ struct LaunchShape {
   int vec;      // columns per thread per iteration (1, 2 or 4)
   int threads;  // workgroup size
   int blocks;   // workgroups (grid-stride loop inside)
+  int batch;    // workers whose loads are issued together (1, 2, 4 or 8)
 };
 
 // Launchers: enqueue on `stream`, return the launch status.

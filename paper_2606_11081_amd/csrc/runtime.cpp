@@ -159,20 +159,22 @@ std::string check_csr(const gasloc_csr& W, int n) {
   return "";
 }
 
-// Workgroup shape of the gossip kernel: the widest vector (4, 2, 1 columns
-// per thread) whose LDS footprint lets at least four workgroups share a CU;
-// narrower workgroups only when even that does not fit one workgroup.
-gasloc::LaunchShape pick_gossip_shape(const gasloc_ctx& c, int nnz_max) {
-  gasloc::LaunchShape s{4, 256, 0};
-  const size_t budget = c.lds_per_cu / 4;
+// Workgroup shape of the gossip kernel.  The z slots of all n workers live
+// in LDS, so LDS bounds the columns in flight per CU; sweeps on the n = 8,
+// 16, 32, 64 workloads found 4-column vectors best up to n = 16 and single
+// columns (more threads in flight) beyond.  The workgroup is the largest
+// whose LDS stays within half a CU's, and loads of 8 workers are batched.
+gasloc::LaunchShape pick_gossip_shape(const gasloc_ctx& c, int nnz) {
+  const size_t budget = std::min(c.lds_per_cu / 2, c.lds_per_block_max);
+  const int widest = c.n <= 16 ? 4 : 1;
   for (int vec : {4, 2, 1}) {
-    s.vec = vec;
-    if (gasloc::gossip_lds_bytes(c.n, nnz_max, s) + gasloc::kStaticLds <= budget) break;
+    if (vec > widest) continue;
+    for (int threads : {256, 128, 64}) {
+      gasloc::LaunchShape s{vec, threads, 0, 8};
+      if (gasloc::gossip_lds_bytes(c.n, nnz, s) + gasloc::kStaticLds <= budget) return s;
+    }
   }
-  while (s.threads > 64 &&
-         gasloc::gossip_lds_bytes(c.n, nnz_max, s) + gasloc::kStaticLds > c.lds_per_block_max)
-    s.threads /= 2;
-  return s;
+  return gasloc::LaunchShape{1, 64, 0, 8};
 }
 
 int gossip_blocks(const gasloc_ctx& c, const gasloc::LaunchShape& s, int nnz) {
@@ -184,16 +186,19 @@ int gossip_blocks(const gasloc_ctx& c, const gasloc::LaunchShape& s, int nnz) {
   return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(needed, int64_t(c.cus) * per_cu)));
 }
 
-// Optional shape override for tuning sweeps: GASLOC_GOSSIP_SHAPE="vec,threads,blocks".
+// Optional shape override for tuning sweeps:
+// GASLOC_GOSSIP_SHAPE="vec,threads,blocks,batch" (blocks 0 = computed).
 void apply_shape_override(gasloc::LaunchShape* s) {
   const char* env = std::getenv("GASLOC_GOSSIP_SHAPE");
   if (!env) return;
-  int v = 0, t = 0, b = 0;
-  if (std::sscanf(env, "%d,%d,%d", &v, &t, &b) == 3 && (v == 1 || v == 2 || v == 4) &&
-      (t == 64 || t == 128 || t == 256) && b >= 0 && b <= kMaxGridBlocks) {
+  int v = 0, t = 0, b = 0, r = 0;
+  if (std::sscanf(env, "%d,%d,%d,%d", &v, &t, &b, &r) == 4 && (v == 1 || v == 2 || v == 4) &&
+      (t == 64 || t == 128 || t == 256) && b >= 0 && b <= kMaxGridBlocks &&
+      (r == 1 || r == 2 || r == 4 || r == 8)) {
     s->vec = v;
     s->threads = t;
-    s->blocks = b;  // 0: keep the computed count
+    s->blocks = b;
+    s->batch = r;
   }
 }
 
@@ -319,7 +324,9 @@ gasloc_status gasloc_init(int32_t n, int64_t P, const gasloc_topology* topology,
     release(c);
     return fail(nullptr, GASLOC_EINVAL, "gossip workgroup does not fit the device's LDS");
   }
-  c->adam_blocks_total = c->cus * 8;
+  // at least two 256-thread workgroups per CU and 32 per active worker:
+  // measured best for the AdamW stream on the n = 8..64 workloads
+  c->adam_blocks_total = c->cus * 2;
   c->reduce_blocks = std::min(kMaxGridBlocks, c->cus * 4);
   c->partial_cap = kMaxGridBlocks;
 
@@ -385,7 +392,12 @@ gasloc_status gasloc_local_step(gasloc_ctx* c, const float* grads, int64_t grad_
   if (slots == 0) return GASLOC_OK;
   a.n_active = slots;
   const int64_t groups = (c->P + 3) / 4;
-  const int64_t want = std::max<int64_t>(1, c->adam_blocks_total / slots);
+  int total_blocks = c->adam_blocks_total;
+  if (const char* env = std::getenv("GASLOC_ADAM_BLOCKS")) {  // tuning sweeps
+    const int b = std::atoi(env);
+    if (b > 0 && b <= 1 << 20) total_blocks = b;
+  }
+  const int64_t want = std::max<int64_t>(32, total_blocks / slots);
   const int per_worker = static_cast<int>(std::min<int64_t>(want, (groups + 255) / 256));
   HIP_TRY(c, gasloc::launch_local_adamw(a, c->hp.param_dtype, per_worker, c->stream));
   for (int s = 0; s < slots; ++s) {
