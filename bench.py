@@ -23,7 +23,8 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, AMD specification
 METRIC = "replica-param updates/s per gossip round; achieved HBM GB/s vs peak"
 DEFAULT_WORKLOAD = "onepeer-exp-n16-p350m"
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2606_11081_amd", "csrc", "kernels.hip")
+# the kernels and the code that picks their launch shapes
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_11081_amd", "csrc", f) for f in ("kernels.hip", "runtime.cpp")]
 
 
 def log(msg):
@@ -31,8 +32,11 @@ def log(msg):
 
 
 def kernels_sha():
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def param_bytes(dtype):
