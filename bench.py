@@ -60,6 +60,15 @@ def gossip_bytes_per_rp(sp, gamma, stepped=True, with_u=True):
     return b
 
 
+def fused_bytes_per_rp(sp, gamma, active, stepped, with_u=True):
+    """Fused last local step + round, per worker: an active worker also reads
+    g, m, v and writes m, v; its new iterate is never stored."""
+    b = gossip_bytes_per_rp(sp, gamma, stepped=stepped, with_u=with_u)
+    if active:
+        b += 4 + 8 + 8
+    return b
+
+
 def read_traffic(kernel, workload):
     """HBM bytes per dispatch from a committed rocprofv3 --pmc summary, or None
     if absent or taken on a different kernel source."""
@@ -111,6 +120,8 @@ def main():
     ap.add_argument("--cpu-columns", type=int, default=24_000_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-gb", type=float, default=8.0, help="size of the copy probe (GB read)")
+    ap.add_argument("--no-fuse", dest="fuse", action="store_false",
+                    help="run the last local step and the round as two calls")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -144,28 +155,35 @@ def main():
     stream = lib.stream
     torch.cuda.synchronize()
 
+    def rec(ev, key, extra=None):
+        pair = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True), extra)
+        ev[key].append(pair)
+        pair[0].record(stream)
+        return pair
+
     def one_round(t, ev=None):
-        for h, act in enumerate(masks):
-            if ev is not None:
-                ev["adam"].append((torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
-                                   int(act.sum())))
-                ev["adam"][-1][0].record(stream)
-            lib.local_step(grads, gi.LOCAL_LR, act)
-            if ev is not None:
-                ev["adam"][-1][1].record(stream)
-        if ev is not None:
-            ev["gossip"].append((torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)))
-            ev["gossip"][-1][0].record(stream)
-        lib.gossip_round(t)
-        if ev is not None:
-            ev["gossip"][-1][1].record(stream)
+        """H_i local steps and the round; the last step is fused into the round."""
+        last = len(masks) - 1 if args.fuse else len(masks)
+        for h in range(last):
+            e = rec(ev, "adam", int(masks[h].sum())) if ev is not None else None
+            lib.local_step(grads, gi.LOCAL_LR, masks[h])
+            if e:
+                e[1].record(stream)
+        if args.fuse:
+            e = rec(ev, "round", masks[-1]) if ev is not None else None
+            lib.local_step_gossip_round(grads, gi.LOCAL_LR, t, masks[-1])
+        else:
+            e = rec(ev, "round", None) if ev is not None else None
+            lib.gossip_round(t)
+        if e:
+            e[1].record(stream)
         return lib.consensus_error()
 
     for t in range(args.warmup):
         one_round(t)
     torch.cuda.synchronize()
 
-    ev = {"adam": [], "gossip": []}
+    ev = {"adam": [], "round": []}
     ces = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -177,12 +195,32 @@ def main():
 
     adam_ms = [a.elapsed_time(b) for a, b, _ in ev["adam"]]
     adam_rp = [k * w.P for _, _, k in ev["adam"]]
-    gossip_ms = [a.elapsed_time(b) for a, b in ev["gossip"]]
+    round_ms = [a.elapsed_time(b) for a, b, _ in ev["round"]]
     adam_bytes = adamw_bytes_per_rp(sp)
+    if args.fuse:
+        act_last = masks[-1]
+        # a worker read y in the fused call if it took a local step earlier this round
+        stepped_before = np.minimum(H_i, len(masks) - 1) > 0
+        round_bytes = sum(fused_bytes_per_rp(sp, w.gamma, bool(act_last[i]), bool(stepped_before[i]))
+                          for i in range(w.n)) * w.P
+    else:
+        round_bytes = w.n * w.P * gossip_bytes_per_rp(sp, w.gamma)
+    adam_gbps = sum(r * adam_bytes for r in adam_rp) / (sum(adam_ms) * 1e-3) / 1e9 if adam_ms else 0.0
+    round_gbps = round_bytes / (np.mean(round_ms) * 1e-3) / 1e9
+    adam_total, round_total = sum(adam_ms), sum(round_ms)
+
+    # the standalone gossip kernel (no fused step), timed after the rounds
+    g_ms = []
+    for s in range(3):
+        lib.local_step(grads, gi.LOCAL_LR)
+        e = rec({"g": []}, "g")
+        lib.gossip_round(args.warmup + args.steps + s)
+        e[1].record(stream)
+        torch.cuda.synchronize()
+        g_ms.append(e[0].elapsed_time(e[1]))
     gossip_bytes = gossip_bytes_per_rp(sp, w.gamma)
-    adam_gbps = sum(r * adam_bytes for r in adam_rp) / (sum(adam_ms) * 1e-3) / 1e9
-    gossip_gbps = w.n * w.P * gossip_bytes / (np.mean(gossip_ms) * 1e-3) / 1e9
-    adam_total, gossip_total = sum(adam_ms), sum(gossip_ms)
+    gossip_ms = float(np.median(g_ms))
+    gossip_gbps = w.n * w.P * gossip_bytes / (gossip_ms * 1e-3) / 1e9
 
     # copy probe: a plain device copy of known size, same run
     copy_elems = int(args.copy_gb * 1e9 / 4)
@@ -198,17 +236,17 @@ def main():
     copy_gbps = 2 * copy_elems * 4 * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9
     del src, dst
 
-    if adam_total >= gossip_total and adam_ms:
-        dom, dom_bytes = "k_local_adamw", np.mean([r * adam_bytes for r in adam_rp])
+    if adam_total >= round_total and adam_ms:
+        dom, dom_bytes = "k_local_adamw", float(np.mean([r * adam_bytes for r in adam_rp]))
         dom_ms = float(np.mean(adam_ms))
     else:
-        dom, dom_bytes, dom_ms = "k_gossip_round", w.n * w.P * gossip_bytes, float(np.mean(gossip_ms))
+        dom = "k_gossip_round" if not args.fuse else "k_gossip_round_fused"
+        dom_bytes, dom_ms = round_bytes, float(np.mean(round_ms))
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
                 "traffic": read_traffic(dom, w.name),
                 "algorithmic_bytes_per_launch": int(dom_bytes), "avg_launch_ms": round(dom_ms, 4)}
-    gossip_rp = w.n * w.P / (np.mean(gossip_ms) * 1e-3)
     out = {
         "metric": METRIC,
         "value": w.n * w.P / (ms_step * 1e-3),
@@ -219,14 +257,20 @@ def main():
         "dtype": w.param_dtype, "data": "synthetic",
         "config": {"workload": w.name, "n": w.n, "P": w.P, "topology": w.topology,
                    "local_steps": "U{%d..%d}" % w.hetero_H if w.hetero_H else w.H,
-                   "gamma": w.gamma, "param_dtype": w.param_dtype, "state_dtype": "f32"},
+                   "gamma": w.gamma, "param_dtype": w.param_dtype, "state_dtype": "f32",
+                   "last_local_step_fused": bool(args.fuse)},
         "roofline": roofline,
-        "gossip_round": {"rp_updates_per_s": gossip_rp, "ms": round(float(np.mean(gossip_ms)), 4),
-                         "GBps": round(gossip_gbps, 1), "frac_of_peak": round(gossip_gbps / PEAK_HBM_GBPS, 4),
-                         "bytes_per_rp": gossip_bytes, "traffic": read_traffic("k_gossip_round", w.name)},
-        "local_adamw": {"ms_per_launch": round(float(np.mean(adam_ms)), 4), "GBps": round(adam_gbps, 1),
-                        "frac_of_peak": round(adam_gbps / PEAK_HBM_GBPS, 4), "bytes_per_rp": adam_bytes,
-                        "launches_per_round": len(masks)},
+        "gossip_round": {"kernel": "k_gossip_round", "rp_updates_per_s": w.n * w.P / (gossip_ms * 1e-3),
+                         "ms": round(gossip_ms, 4), "GBps": round(gossip_gbps, 1),
+                         "frac_of_peak": round(gossip_gbps / PEAK_HBM_GBPS, 4), "bytes_per_rp": gossip_bytes,
+                         "traffic": read_traffic("k_gossip_round", w.name)},
+        "round_kernel": {"kernel": "k_gossip_round_fused" if args.fuse else "k_gossip_round",
+                         "ms": round(float(np.mean(round_ms)), 4), "GBps": round(round_gbps, 1),
+                         "frac_of_peak": round(round_gbps / PEAK_HBM_GBPS, 4),
+                         "bytes_per_launch": int(round_bytes)},
+        "local_adamw": {"ms_per_launch": round(float(np.mean(adam_ms)), 4) if adam_ms else None,
+                        "GBps": round(adam_gbps, 1), "frac_of_peak": round(adam_gbps / PEAK_HBM_GBPS, 4),
+                        "bytes_per_rp": adam_bytes, "launches_per_round": len(adam_ms) // max(args.steps, 1)},
         "copy_probe_GBps": round(copy_gbps, 1),
         "consensus_error_last": ces[-1],
     }

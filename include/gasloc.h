@@ -18,8 +18,8 @@
  *   - "device" pointers are HIP device memory on the GPU that is current
  *     when gasloc_init runs; "host" pointers are ordinary CPU memory.
  *   - All device work is enqueued on the stream given to gasloc_init.  Only
- *     gasloc_consensus_error*, gasloc_topology_csr (none) and gasloc_destroy
- *     block the host; kernel faults surface at the next blocking call.
+ *     gasloc_consensus_error, gasloc_consensus_error_cols and gasloc_destroy
+ *     wait for the stream; kernel faults surface at the next blocking call.
  *   - A context is not thread-safe; distinct contexts are independent.
  *   - After a device error every call on the context returns GASLOC_ESTATE.
  */
@@ -124,7 +124,7 @@ typedef struct gasloc_ctx gasloc_ctx;
 
 /* Create a context for n in [1, 64] workers of P in [1, 2^31) parameters.
  * Validates the arguments, allocates the context's own small device scratch
- * (CSR double buffer, reduction partials) and pinned staging, zeroes m, v,
+ * (one CSR buffer, reduction partials) and a pinned CSR staging ring, zeroes m, v,
  * u, zp and the step counters on `hip_stream` (a hipStream_t; NULL = the
  * null stream).  The caller then fills x (and may leave y uninitialised):
  * y is logically equal to x until the first local step (identical start,
@@ -161,6 +161,19 @@ gasloc_status gasloc_local_step(gasloc_ctx *ctx, const float *grads, int64_t gra
  * step since the last round has delta = 0.  Enqueues two kernels and one
  * host-to-device copy of the CSR (at most 33 KB). */
 gasloc_status gasloc_gossip_round(gasloc_ctx *ctx, const gasloc_csr *W, uint64_t t);
+
+/* One local step immediately followed by the gossip round, in a single pass
+ * over HBM: the same results as gasloc_local_step(grads, grad_ld, active, lr)
+ * then gasloc_gossip_round(W, t), bit for bit, but the new local iterate of
+ * the stepping workers feeds the pseudo-gradient from registers and is never
+ * stored (the round resets it to the new x anyway, Eq. 1: x_{t+1,0} =
+ * x_{t+1}).  Use it for the last local step of a round (Algorithm 1: the
+ * inner loop ends with y_i = x_i^{(t,H_i)}).  Saves 8 bytes per fp32
+ * replica-parameter (12 when H_i = 1).  Same argument rules as the two calls;
+ * enqueues two kernels and one CSR copy. */
+gasloc_status gasloc_local_step_gossip_round(gasloc_ctx *ctx, const float *grads, int64_t grad_ld,
+                                             const uint8_t *active, float lr, const gasloc_csr *W,
+                                             uint64_t t);
 
 /* ||pi x||^2 = sum_p sum_i (x_ip - xbar_p)^2 over the stored x (fp64
  * result).  Uses the value fused into the last gossip round when it is

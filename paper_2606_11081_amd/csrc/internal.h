@@ -57,6 +57,19 @@ struct GossipArgs {
   int32_t apply_gamma;  // gamma term of Eq. 2 (not in the first round)
   int32_t store_zp;     // keep z for the next round's gamma term
   uint64_t stepped;     // bit i: worker i took local steps since the last round
+
+  // Fused last local step (the fused kernel only): every worker i with bit i
+  // of `active` first takes one AdamW step from its live iterate; the new
+  // iterate feeds delta directly and is never written back (it is logically
+  // reset to the new x by the round).  Scalars are indexed by worker.
+  const float* g;
+  float* m;
+  float* v;
+  int64_t gld;
+  uint64_t active;
+  float c_wd, b1, omb1, b2, omb2, eps;
+  float s1[kMaxReplicas];
+  float c2[kMaxReplicas];
 };
 
 struct LaunchShape {
@@ -68,7 +81,7 @@ struct LaunchShape {
 
 // Launchers: enqueue on `stream`, return the launch status.
 hipError_t launch_local_adamw(const AdamArgs& a, int dtype, int blocks_per_worker, hipStream_t stream);
-hipError_t launch_gossip_round(const GossipArgs& a, int dtype, const LaunchShape& shape,
+hipError_t launch_gossip_round(const GossipArgs& a, int dtype, bool fused, const LaunchShape& shape,
                                hipStream_t stream);
 hipError_t launch_consensus_error(const void* x, int dtype, int64_t ld, int n, int64_t p_begin,
                                   int64_t p_end, double* partials, int blocks, hipStream_t stream);

@@ -163,6 +163,15 @@ __device__ __forceinline__ void store_params(void* base, int64_t idx, int cnt, c
   }
 }
 
+// The value a store to the parameter dtype keeps (RNE to bf16, or fp32 as is).
+template <int DT>
+__device__ __forceinline__ float as_stored(float v) {
+  if constexpr (DT == GASLOC_BF16)
+    return bf16_to_f32(f32_to_bf16(v));
+  else
+    return v;
+}
+
 // ---------------------------------------------------------------------------
 // reductions: fixed-order wave shuffle, then the waves of the workgroup
 // ---------------------------------------------------------------------------
@@ -248,7 +257,7 @@ struct CsrEntry {
   float val;
 };
 
-template <int DT, int V, int R>
+template <int DT, int V, int R, bool FUSED>
 __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int n = a.n;
@@ -273,10 +282,13 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
     const int64_t p = gi * V;
     const int cnt = static_cast<int>(a.P - p < V ? a.P - p : V);
 
-    // phase 1: delta = x - y, outer (Nesterov / heavy-ball) step -> z.
-    // The loads of R workers are issued together before any of them is used.
+    // phase 1: [fused: last AdamW step ->] delta = x - y, outer (Nesterov /
+    // heavy-ball) step -> z.  The loads of R workers are issued together
+    // before any of them is used.
     for (int i0 = 0; i0 < n; i0 += R) {
+      constexpr int RF = FUSED ? R : 1;
       float xv[R][V], yv[R][V], uv[R][V];
+      float gv[RF][V], mv[RF][V], vv[RF][V];
 #pragma unroll
       for (int r = 0; r < R; ++r) {
         const int i = i0 + r;
@@ -288,6 +300,13 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
         } else {
 #pragma unroll
           for (int c = 0; c < V; ++c) yv[r][c] = xv[r][c];
+        }
+        if constexpr (FUSED) {
+          if ((a.active >> i) & 1ull) {
+            load_f32<V>(a.g + static_cast<int64_t>(i) * a.gld + p, cnt, gv[r]);
+            load_f32<V>(a.m + e, cnt, mv[r]);
+            load_f32<V>(a.v + e, cnt, vv[r]);
+          }
         }
         if (a.use_u) {
           load_f32<V>(a.u + e, cnt, uv[r]);
@@ -301,6 +320,17 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
         const int i = i0 + r;
         if (i >= n) break;
         const int64_t e = static_cast<int64_t>(i) * a.ld + p;
+        if constexpr (FUSED) {
+          if ((a.active >> i) & 1ull) {
+            const float s1 = a.s1[i], c2 = a.c2[i];
+#pragma unroll
+            for (int c = 0; c < V; ++c)
+              yv[r][c] = as_stored<DT>(adamw_element(yv[r][c], gv[r][c], mv[r][c], vv[r][c], a.c_wd, a.b1,
+                                                     a.omb1, a.b2, a.omb2, a.eps, s1, c2));
+            store_f32<V>(a.m + e, cnt, mv[r]);
+            store_f32<V>(a.v + e, cnt, vv[r]);
+          }
+        }
         float z[V];
 #pragma unroll
         for (int c = 0; c < V; ++c) {
@@ -434,21 +464,32 @@ __global__ __launch_bounds__(256) void k_replica_mean(const void* x, int64_t ld,
   }
 }
 
-template <int DT, int V, int R>
+template <int DT, int V, int R, bool FUSED>
 hipError_t launch_gossip_typed(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
   const size_t lds = gossip_lds_bytes(a.n, a.nnz, s);
-  hipLaunchKernelGGL((k_gossip_round<DT, V, R>), dim3(s.blocks), dim3(s.threads), lds, stream, a);
+  hipLaunchKernelGGL((k_gossip_round<DT, V, R, FUSED>), dim3(s.blocks), dim3(s.threads), lds, stream, a);
   return hipGetLastError();
 }
 
-template <int DT, int V>
+// The fused kernel carries three more streams per worker, so it batches at
+// most 4 workers to stay within the register file.
+template <int DT, int V, bool FUSED>
 hipError_t launch_gossip_batched(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
   switch (s.batch) {
-    case 1: return launch_gossip_typed<DT, V, 1>(a, s, stream);
-    case 2: return launch_gossip_typed<DT, V, 2>(a, s, stream);
-    case 8: return launch_gossip_typed<DT, V, 8>(a, s, stream);
-    default: return launch_gossip_typed<DT, V, 4>(a, s, stream);
+    case 1: return launch_gossip_typed<DT, V, 1, FUSED>(a, s, stream);
+    case 2: return launch_gossip_typed<DT, V, 2, FUSED>(a, s, stream);
+    case 8:
+      if constexpr (!FUSED) return launch_gossip_typed<DT, V, 8, FUSED>(a, s, stream);
+      [[fallthrough]];
+    default: return launch_gossip_typed<DT, V, 4, FUSED>(a, s, stream);
   }
+}
+
+template <int DT, bool FUSED>
+hipError_t launch_gossip_dtype(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
+  if (s.vec == 4) return launch_gossip_batched<DT, 4, FUSED>(a, s, stream);
+  if (s.vec == 2) return launch_gossip_batched<DT, 2, FUSED>(a, s, stream);
+  return launch_gossip_batched<DT, 1, FUSED>(a, s, stream);
 }
 
 }  // namespace
@@ -469,15 +510,13 @@ hipError_t launch_local_adamw(const AdamArgs& a, int dtype, int blocks_per_worke
   return hipGetLastError();
 }
 
-hipError_t launch_gossip_round(const GossipArgs& a, int dtype, const LaunchShape& s, hipStream_t stream) {
-  if (dtype == GASLOC_BF16) {
-    if (s.vec == 4) return launch_gossip_batched<GASLOC_BF16, 4>(a, s, stream);
-    if (s.vec == 2) return launch_gossip_batched<GASLOC_BF16, 2>(a, s, stream);
-    return launch_gossip_batched<GASLOC_BF16, 1>(a, s, stream);
-  }
-  if (s.vec == 4) return launch_gossip_batched<GASLOC_F32, 4>(a, s, stream);
-  if (s.vec == 2) return launch_gossip_batched<GASLOC_F32, 2>(a, s, stream);
-  return launch_gossip_batched<GASLOC_F32, 1>(a, s, stream);
+hipError_t launch_gossip_round(const GossipArgs& a, int dtype, bool fused, const LaunchShape& s,
+                               hipStream_t stream) {
+  if (dtype == GASLOC_BF16)
+    return fused ? launch_gossip_dtype<GASLOC_BF16, true>(a, s, stream)
+                 : launch_gossip_dtype<GASLOC_BF16, false>(a, s, stream);
+  return fused ? launch_gossip_dtype<GASLOC_F32, true>(a, s, stream)
+               : launch_gossip_dtype<GASLOC_F32, false>(a, s, stream);
 }
 
 hipError_t launch_consensus_error(const void* x, int dtype, int64_t ld, int n, int64_t p_begin,

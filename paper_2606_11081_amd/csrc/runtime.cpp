@@ -248,6 +248,139 @@ gasloc_status read_ce(gasloc_ctx* c, double* out) {
   return GASLOC_OK;
 }
 
+// One local AdamW step, planned on the host: the workers it moves and their
+// scalars for step number k_i + 1, evaluated in fp64 and rounded once.
+struct StepPlan {
+  uint64_t active = 0;
+  int count = 0;
+  float c_wd = 0, b1 = 0, b2 = 0, omb1 = 0, omb2 = 0, eps = 0;
+  float s1[kMaxReplicas] = {};
+  float c2[kMaxReplicas] = {};
+};
+
+gasloc_status check_step(gasloc_ctx* c, const float* grads, int64_t grad_ld, float lr) {
+  if (!grads || !aligned16(grads)) return fail(c, GASLOC_EINVAL, "grads must be non-NULL and 16-byte aligned");
+  if (grad_ld < c->P || (grad_ld * 4) % 16 != 0)
+    return fail(c, GASLOC_EINVAL, "grad_ld must be >= P and a multiple of 4");
+  if (!(std::isfinite(lr) && lr >= 0.0f)) return fail(c, GASLOC_EINVAL, "lr must be finite and >= 0");
+  return GASLOC_OK;
+}
+
+StepPlan plan_step(const gasloc_ctx& c, const uint8_t* active, float lr) {
+  StepPlan s;
+  const double lr64 = lr, b1 = c.hp.beta1, b2 = c.hp.beta2;
+  s.c_wd = static_cast<float>(1.0 - lr64 * static_cast<double>(c.hp.weight_decay));
+  s.b1 = c.hp.beta1;
+  s.b2 = c.hp.beta2;
+  s.omb1 = static_cast<float>(1.0 - b1);
+  s.omb2 = static_cast<float>(1.0 - b2);
+  s.eps = c.hp.eps;
+  for (int i = 0; i < c.n; ++i) {
+    if (active && !active[i]) continue;
+    const double k = static_cast<double>(c.k[static_cast<size_t>(i)] + 1);
+    s.s1[i] = static_cast<float>(lr64 / (1.0 - std::pow(b1, k)));
+    s.c2[i] = static_cast<float>(std::sqrt(1.0 - std::pow(b2, k)));
+    s.active |= 1ull << i;
+    ++s.count;
+  }
+  return s;
+}
+
+void commit_step(gasloc_ctx* c, const StepPlan& s) {
+  for (int i = 0; i < c->n; ++i) {
+    if (!((s.active >> i) & 1ull)) continue;
+    c->k[static_cast<size_t>(i)] += 1;
+    c->stepped[static_cast<size_t>(i)] = 1;
+  }
+}
+
+// A gossip round, optionally preceded in the same kernel by one local step of
+// the workers in `step` (then `grads` holds their gradients).
+gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const StepPlan* step,
+                        const float* grads, int64_t grad_ld) {
+  const int32_t *rp, *col;
+  const float* val;
+  int32_t nnz = 0;
+  if (W) {
+    const std::string e = check_csr(*W, c->n);
+    if (!e.empty()) return fail(c, GASLOC_EINVAL, e);
+    rp = W->row_ptr;
+    col = W->col;
+    val = W->val;
+    nnz = W->nnz;
+  } else {
+    if (c->topo.kind == GASLOC_TOPO_EXPLICIT)
+      return fail(c, GASLOC_EINVAL, "EXPLICIT topology: pass W to every round");
+    std::string err;
+    if (!gasloc::make_topology(c->topo, c->n, t, c->row_ptr.data(), c->col.data(), c->val.data(),
+                               c->n * c->n, &nnz, &err))
+      return fail(c, GASLOC_EINVAL, "topology: " + err);
+    rp = c->row_ptr.data();
+    col = c->col.data();
+    val = c->val.data();
+  }
+  DeviceGuard guard(c->device);
+  gasloc::LaunchShape shape = pick_gossip_shape(*c, nnz);
+  if (step) shape.batch = 4;
+  shape.blocks = gossip_blocks(*c, shape, nnz);
+  apply_shape_override(&shape);
+  if (shape.blocks == 0) shape.blocks = gossip_blocks(*c, shape, nnz);
+  shape.blocks = std::min(shape.blocks, c->partial_cap);
+  if (gasloc::gossip_lds_bytes(c->n, nnz, shape) + gasloc::kStaticLds > c->lds_per_block_max)
+    return fail(c, GASLOC_EINVAL, "gossip shape exceeds the device's LDS per workgroup");
+  gasloc_status st = upload_csr(c, rp, col, val, nnz);
+  if (st != GASLOC_OK) return st;
+
+  gasloc::GossipArgs a{};
+  a.x = c->buf.x;
+  a.y = c->buf.y;
+  a.u = c->buf.u;
+  a.zp = c->buf.zp;
+  const size_t rp_bytes = sizeof(int32_t) * static_cast<size_t>(c->n + 1);
+  a.row_ptr = reinterpret_cast<const int32_t*>(c->d_csr);
+  a.col = reinterpret_cast<const int32_t*>(c->d_csr + rp_bytes);
+  a.val = reinterpret_cast<const float*>(c->d_csr + rp_bytes + sizeof(int32_t) * c->n * c->n);
+  a.ld = c->buf.ld;
+  a.P = c->P;
+  a.n = c->n;
+  a.nnz = nnz;
+  a.mu = c->hp.outer_momentum;
+  a.eta = c->hp.outer_lr;
+  a.gamma = c->hp.consensus_momentum;
+  a.nesterov = c->hp.outer_nesterov;
+  a.use_u = c->buf.u != nullptr;
+  a.store_zp = c->hp.consensus_momentum != 0.0f;
+  a.apply_gamma = a.store_zp && c->rounds_done > 0;
+  for (int i = 0; i < c->n; ++i)
+    if (c->stepped[static_cast<size_t>(i)]) a.stepped |= (1ull << i);
+  if (step) {
+    a.g = grads;
+    a.gld = grad_ld;
+    a.m = c->buf.m;
+    a.v = c->buf.v;
+    a.active = step->active;
+    a.c_wd = step->c_wd;
+    a.b1 = step->b1;
+    a.b2 = step->b2;
+    a.omb1 = step->omb1;
+    a.omb2 = step->omb2;
+    a.eps = step->eps;
+    std::memcpy(a.s1, step->s1, sizeof a.s1);
+    std::memcpy(a.c2, step->c2, sizeof a.c2);
+  }
+  a.partials = c->d_partials;
+  HIP_TRY(c, gasloc::launch_gossip_round(a, c->hp.param_dtype, step != nullptr, shape, c->stream));
+  HIP_TRY(c, gasloc::launch_finalize(c->d_partials, shape.blocks, c->d_ce, c->stream));
+  if (step) {
+    for (int i = 0; i < c->n; ++i)
+      if ((step->active >> i) & 1ull) c->k[static_cast<size_t>(i)] += 1;
+  }
+  c->rounds_done += 1;
+  std::fill(c->stepped.begin(), c->stepped.end(), 0);
+  c->ce_current = true;
+  return GASLOC_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -357,11 +490,11 @@ gasloc_status gasloc_local_step(gasloc_ctx* c, const float* grads, int64_t grad_
                                 float lr) {
   if (!c) return fail(nullptr, GASLOC_EINVAL, "NULL context");
   if (c->failed) return fail(c, GASLOC_ESTATE, "context unusable after a device error: " + c->err);
-  if (!grads || !aligned16(grads)) return fail(c, GASLOC_EINVAL, "grads must be non-NULL and 16-byte aligned");
-  if (grad_ld < c->P || (grad_ld * 4) % 16 != 0)
-    return fail(c, GASLOC_EINVAL, "grad_ld must be >= P and a multiple of 4");
-  if (!(std::isfinite(lr) && lr >= 0.0f)) return fail(c, GASLOC_EINVAL, "lr must be finite and >= 0");
+  gasloc_status st = check_step(c, grads, grad_ld, lr);
+  if (st != GASLOC_OK) return st;
   DeviceGuard guard(c->device);
+  const StepPlan plan = plan_step(*c, active, lr);
+  if (plan.count == 0) return GASLOC_OK;
 
   gasloc::AdamArgs a{};
   a.x = c->buf.x;
@@ -372,106 +505,53 @@ gasloc_status gasloc_local_step(gasloc_ctx* c, const float* grads, int64_t grad_
   a.ld = c->buf.ld;
   a.gld = grad_ld;
   a.P = c->P;
-  const double lr64 = lr, b1 = c->hp.beta1, b2 = c->hp.beta2;
-  a.c_wd = static_cast<float>(1.0 - lr64 * static_cast<double>(c->hp.weight_decay));
-  a.b1 = c->hp.beta1;
-  a.b2 = c->hp.beta2;
-  a.omb1 = static_cast<float>(1.0 - b1);
-  a.omb2 = static_cast<float>(1.0 - b2);
-  a.eps = c->hp.eps;
+  a.c_wd = plan.c_wd;
+  a.b1 = plan.b1;
+  a.b2 = plan.b2;
+  a.omb1 = plan.omb1;
+  a.omb2 = plan.omb2;
+  a.eps = plan.eps;
   int slots = 0;
   for (int i = 0; i < c->n; ++i) {
-    if (active && !active[i]) continue;
-    const int64_t k = c->k[static_cast<size_t>(i)] + 1;
+    if (!((plan.active >> i) & 1ull)) continue;
     a.rep[slots] = i;
-    a.s1[slots] = static_cast<float>(lr64 / (1.0 - std::pow(b1, static_cast<double>(k))));
-    a.c2[slots] = static_cast<float>(std::sqrt(1.0 - std::pow(b2, static_cast<double>(k))));
+    a.s1[slots] = plan.s1[i];
+    a.c2[slots] = plan.c2[i];
     if (!c->stepped[static_cast<size_t>(i)]) a.from_x |= (1ull << slots);
     ++slots;
   }
-  if (slots == 0) return GASLOC_OK;
   a.n_active = slots;
   const int64_t groups = (c->P + 3) / 4;
   int total_blocks = c->adam_blocks_total;
+  int64_t floor_per_worker = 32;
   if (const char* env = std::getenv("GASLOC_ADAM_BLOCKS")) {  // tuning sweeps
     const int b = std::atoi(env);
-    if (b > 0 && b <= 1 << 20) total_blocks = b;
+    if (b > 0 && b <= 1 << 20) {
+      total_blocks = b;
+      floor_per_worker = 1;
+    }
   }
-  const int64_t want = std::max<int64_t>(32, total_blocks / slots);
-  const int per_worker = static_cast<int>(std::min<int64_t>(want, (groups + 255) / 256));
+  const int64_t want = std::max<int64_t>(floor_per_worker, total_blocks / slots);
+  const int per_worker = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(want, (groups + 255) / 256)));
   HIP_TRY(c, gasloc::launch_local_adamw(a, c->hp.param_dtype, per_worker, c->stream));
-  for (int s = 0; s < slots; ++s) {
-    c->k[static_cast<size_t>(a.rep[s])] += 1;
-    c->stepped[static_cast<size_t>(a.rep[s])] = 1;
-  }
+  commit_step(c, plan);
   return GASLOC_OK;
 }
 
 gasloc_status gasloc_gossip_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t) {
   if (!c) return fail(nullptr, GASLOC_EINVAL, "NULL context");
   if (c->failed) return fail(c, GASLOC_ESTATE, "context unusable after a device error: " + c->err);
-  const int32_t *rp, *col;
-  const float* val;
-  int32_t nnz = 0;
-  if (W) {
-    const std::string e = check_csr(*W, c->n);
-    if (!e.empty()) return fail(c, GASLOC_EINVAL, e);
-    rp = W->row_ptr;
-    col = W->col;
-    val = W->val;
-    nnz = W->nnz;
-  } else {
-    if (c->topo.kind == GASLOC_TOPO_EXPLICIT)
-      return fail(c, GASLOC_EINVAL, "EXPLICIT topology: pass W to every round");
-    std::string err;
-    if (!gasloc::make_topology(c->topo, c->n, t, c->row_ptr.data(), c->col.data(), c->val.data(),
-                               c->n * c->n, &nnz, &err))
-      return fail(c, GASLOC_EINVAL, "topology: " + err);
-    rp = c->row_ptr.data();
-    col = c->col.data();
-    val = c->val.data();
-  }
-  DeviceGuard guard(c->device);
-  gasloc_status st = upload_csr(c, rp, col, val, nnz);
+  return run_round(c, W, t, nullptr, nullptr, 0);
+}
+
+gasloc_status gasloc_local_step_gossip_round(gasloc_ctx* c, const float* grads, int64_t grad_ld,
+                                             const uint8_t* active, float lr, const gasloc_csr* W, uint64_t t) {
+  if (!c) return fail(nullptr, GASLOC_EINVAL, "NULL context");
+  if (c->failed) return fail(c, GASLOC_ESTATE, "context unusable after a device error: " + c->err);
+  gasloc_status st = check_step(c, grads, grad_ld, lr);
   if (st != GASLOC_OK) return st;
-
-  gasloc::GossipArgs a{};
-  a.x = c->buf.x;
-  a.y = c->buf.y;
-  a.u = c->buf.u;
-  a.zp = c->buf.zp;
-  const size_t rp_bytes = sizeof(int32_t) * static_cast<size_t>(c->n + 1);
-  a.row_ptr = reinterpret_cast<const int32_t*>(c->d_csr);
-  a.col = reinterpret_cast<const int32_t*>(c->d_csr + rp_bytes);
-  a.val = reinterpret_cast<const float*>(c->d_csr + rp_bytes + sizeof(int32_t) * c->n * c->n);
-  a.ld = c->buf.ld;
-  a.P = c->P;
-  a.n = c->n;
-  a.nnz = nnz;
-  a.mu = c->hp.outer_momentum;
-  a.eta = c->hp.outer_lr;
-  a.gamma = c->hp.consensus_momentum;
-  a.nesterov = c->hp.outer_nesterov;
-  a.use_u = c->buf.u != nullptr;
-  a.store_zp = c->hp.consensus_momentum != 0.0f;
-  a.apply_gamma = a.store_zp && c->rounds_done > 0;
-  for (int i = 0; i < c->n; ++i)
-    if (c->stepped[static_cast<size_t>(i)]) a.stepped |= (1ull << i);
-
-  gasloc::LaunchShape shape = pick_gossip_shape(*c, nnz);
-  shape.blocks = gossip_blocks(*c, shape, nnz);
-  apply_shape_override(&shape);
-  if (shape.blocks == 0) shape.blocks = gossip_blocks(*c, shape, nnz);
-  shape.blocks = std::min(shape.blocks, c->partial_cap);
-  if (gasloc::gossip_lds_bytes(c->n, nnz, shape) + gasloc::kStaticLds > c->lds_per_block_max)
-    return fail(c, GASLOC_EINVAL, "gossip shape exceeds the device's LDS per workgroup");
-  a.partials = c->d_partials;
-  HIP_TRY(c, gasloc::launch_gossip_round(a, c->hp.param_dtype, shape, c->stream));
-  HIP_TRY(c, gasloc::launch_finalize(c->d_partials, shape.blocks, c->d_ce, c->stream));
-  c->rounds_done += 1;
-  std::fill(c->stepped.begin(), c->stepped.end(), 0);
-  c->ce_current = true;
-  return GASLOC_OK;
+  const StepPlan plan = plan_step(*c, active, lr);
+  return run_round(c, W, t, plan.count ? &plan : nullptr, grads, grad_ld);
 }
 
 gasloc_status gasloc_consensus_error(gasloc_ctx* c, double* out) {

@@ -63,6 +63,8 @@ _SIGNATURES = {
                                    ctypes.POINTER(_vp)]),
     "gasloc_local_step": (ctypes.c_int, [_vp, _vp, _i64, _vp, ctypes.c_float]),
     "gasloc_gossip_round": (ctypes.c_int, [_vp, ctypes.POINTER(gasloc_csr), _u64]),
+    "gasloc_local_step_gossip_round": (ctypes.c_int, [_vp, _vp, _i64, _vp, ctypes.c_float,
+                                                      ctypes.POINTER(gasloc_csr), _u64]),
     "gasloc_consensus_error": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_double)]),
     "gasloc_consensus_error_cols": (ctypes.c_int, [_vp, _i64, _i64, ctypes.POINTER(ctypes.c_double)]),
     "gasloc_replica_mean": (ctypes.c_int, [_vp, _vp]),
@@ -165,6 +167,21 @@ def gasloc_gossip_round(ctx, W=None, t=0):
     csr, keep = make_csr(*W)
     _check(library().gasloc_gossip_round(ctx, ctypes.byref(csr), int(t)), ctx)
     del keep
+
+
+def gasloc_local_step_gossip_round(ctx, grads, grad_ld, active=None, lr=0.0, W=None, t=0):
+    """The last local step and the gossip round in one pass (same results as the two calls)."""
+    keep_a = ap = None
+    if active is not None:
+        keep_a, ap = _host(active, np.uint8)
+    if W is None:
+        st = library().gasloc_local_step_gossip_round(ctx, _dev(grads), int(grad_ld), ap, float(lr), None, int(t))
+    else:
+        csr, keep = make_csr(*W)
+        st = library().gasloc_local_step_gossip_round(ctx, _dev(grads), int(grad_ld), ap, float(lr),
+                                                      ctypes.byref(csr), int(t))
+    _check(st, ctx)
+    del keep_a
 
 
 def gasloc_consensus_error(ctx):
@@ -289,6 +306,9 @@ class GASLoC:
 
     def gossip_round(self, t, W=None):
         gasloc_gossip_round(self.ctx, W, t)
+
+    def local_step_gossip_round(self, grads, lr, t, active=None, W=None):
+        gasloc_local_step_gossip_round(self.ctx, grads, grads.shape[1], active, lr, W, t)
 
     def consensus_error(self):
         return gasloc_consensus_error(self.ctx)

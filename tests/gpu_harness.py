@@ -102,6 +102,20 @@ class Pair:
             o.local_step(g_host, self.lr, active)
         self.step += 1
 
+    def local_step_gossip_round(self, t, active=None, W=None):
+        """The fused entry on the GPU; the oracle takes the two steps in turn."""
+        gi.fill_grads(self.grads, self.mu_i, self.step)
+        g_host = self.grads[:, self.cols_dev].cpu().numpy()
+        self.gpu.local_step_gossip_round(self.grads, self.lr, t, active, W)
+        for o in self.oracles.values():
+            o.local_step(g_host, self.lr, active)
+            if W is None:
+                o.gossip_round(t)
+            else:
+                rp, col, val = W
+                o.gossip_round(t, csr=(rp, col, val.astype(o.real)))
+        self.step += 1
+
     def gossip_round(self, t, W=None):
         self.gpu.gossip_round(t, W)
         for o in self.oracles.values():

@@ -101,6 +101,50 @@ def test_small_cases(n, P, topology, dtype, H, gamma, mu, nesterov):
         assert pair.gpu.consensus_error() == 0.0
 
 
+FUSED = [
+    # n, P, topology, dtype, H, gamma
+    (4, 1_048_576, "ring", "f32", 1, 0.1),
+    (16, 100_003, "one_peer_exp", "f32", 3, 0.1),
+    (8, 65_537, "exponential", "bf16", 2, 0.1),
+    (64, 20_011, "one_peer", "f32", 2, 0.0),
+    (33, 9_999, "two_peer", "bf16", 1, 0.2),
+]
+
+
+@pytest.mark.parametrize("n,P,topology,dtype,H,gamma", FUSED)
+def test_fused_last_step_matches_two_calls_and_oracle(n, P, topology, dtype, H, gamma):
+    import torch
+
+    log("case fused n=%d P=%d %s %s H=%d gamma=%g" % (n, P, topology, dtype, H, gamma))
+    H_i = np.full(n, H)
+    if n >= 5:
+        H_i[2] = 0
+        H_i[3] = max(1, H - 1)
+    fused = Pair(n, P, topology, dtype, gamma=gamma, precisions=("f32",))
+    split = Pair(n, P, topology, dtype, gamma=gamma, precisions=())
+    for t in range(3):
+        for h in range(int(H_i.max())):
+            act = (H_i > h).astype(np.uint8)
+            split.local_step(active=act)
+            if h == int(H_i.max()) - 1:
+                fused.local_step_gossip_round(t, active=act)
+            else:
+                fused.local_step(active=act)
+        split.gossip_round(t)
+        ce_f, ce_s = fused.gpu.consensus_error(), split.gpu.consensus_error()
+        assert ce_f == ce_s
+        reduction_close(ce_f, fused.oracles["f32"].consensus_error(), "fused CE round %d" % t)
+    torch.cuda.synchronize()
+    for name in ("x", "m", "v", "u", "zp"):
+        a, b = getattr(fused.gpu, name), getattr(split.gpu, name)
+        if a is None:
+            continue
+        assert torch.equal(a[:, :P], b[:, :P]), name
+    assert all(np.array_equal(u, v) for u, v in zip(fused.gpu.counters(), split.gpu.counters()))
+    stats = fused.check_state(tag="fused")
+    log("bit-exact fraction vs fp32 oracle: %s" % stats)
+
+
 def test_explicit_nonsymmetric_csr_and_identity():
     n, P = 6, 5003
     rng = np.random.default_rng(3)
