@@ -441,6 +441,108 @@ int orc_gossip_round(int n, int64_t P, int64_t ld, int dtype, void *x, void *y, 
 }
 
 /* ------------------------------------------------------------------------ */
+/* Other round forms.                                                       */
+/* ------------------------------------------------------------------------ */
+
+static int csr_ok(int n, const int32_t *row_ptr, const int32_t *col) {
+  if (row_ptr[0] != 0) return 0;
+  for (int i = 0; i < n; ++i) {
+    if (row_ptr[i + 1] < row_ptr[i]) return 0;
+    for (int32_t kk = row_ptr[i]; kk < row_ptr[i + 1]; ++kk)
+      if (col[kk] < 0 || col[kk] >= n) return 0;
+  }
+  return 1;
+}
+
+/* The outer optimizer step of a worker: momentum u <- mu u + d, then
+ * base - eta (d + mu u) (Nesterov) or base - eta u (heavy ball). */
+static REAL outer_step(REAL base, REAL d, REAL *u, REAL mur, REAL etar, int nesterov) {
+  *u = mur * *u + d;
+  REAL step = nesterov ? d + mur * *u : *u;
+  return base - etar * step;
+}
+
+/* Algorithm 1: every worker feeds the neighbourhood average of
+ * (x_i - y_j) to its outer optimizer,
+ *   delta_i = sum_k W_ik (x_i - y_{col_k}),  x_i <- OuterOpt(x_i, delta_i),
+ * then the next inner loop starts from x_i (y_i = x_i).  No consensus
+ * momentum in this form. */
+int orc_alg1_round(int n, int64_t P, int64_t ld, int dtype, void *x, void *y, REAL *u,
+                   const int32_t *row_ptr, const int32_t *col, const REAL *val, double mu, double eta,
+                   int nesterov) {
+  if (n < 1 || P < 0 || ld < P || !dtype_ok(dtype) || !csr_ok(n, row_ptr, col)) return -1;
+  const REAL mur = (REAL)mu, etar = (REAL)eta;
+  for (int i = 0; i < n; ++i) {
+    for (int64_t p = 0; p < P; ++p) {
+      int64_t e = (int64_t)i * ld + p;
+      REAL xi = load_param(x, dtype, e);
+      REAL delta = 0;
+      for (int32_t kk = row_ptr[i]; kk < row_ptr[i + 1]; ++kk)
+        delta = delta + val[kk] * (xi - load_param(y, dtype, (int64_t)col[kk] * ld + p));
+      store_param(x, dtype, e, outer_step(xi, delta, &u[e], mur, etar, nesterov));
+    }
+  }
+  /* row i read x_i and the y_j only, so updating x in place above is exact */
+  for (int i = 0; i < n; ++i)
+    for (int64_t p = 0; p < P; ++p) {
+      int64_t e = (int64_t)i * ld + p;
+      store_param(y, dtype, e, load_param(x, dtype, e));
+    }
+  return 0;
+}
+
+/* DAdam step (App. C): mix the pre-update parameters and add the local
+ * displacement,  x_i <- sum_j w_ij x_j + (y_i - x_i).  z: [n, ld] scratch. */
+int orc_dadam_round(int n, int64_t P, int64_t ld, int dtype, void *x, void *y, REAL *z,
+                    const int32_t *row_ptr, const int32_t *col, const REAL *val) {
+  if (n < 1 || P < 0 || ld < P || !dtype_ok(dtype) || !csr_ok(n, row_ptr, col)) return -1;
+  for (int i = 0; i < n; ++i) {
+    for (int64_t p = 0; p < P; ++p) {
+      int64_t e = (int64_t)i * ld + p;
+      REAL acc = 0;
+      for (int32_t kk = row_ptr[i]; kk < row_ptr[i + 1]; ++kk)
+        acc = acc + val[kk] * load_param(x, dtype, (int64_t)col[kk] * ld + p);
+      z[e] = acc + (load_param(y, dtype, e) - load_param(x, dtype, e));
+    }
+  }
+  for (int i = 0; i < n; ++i)
+    for (int64_t p = 0; p < P; ++p) {
+      int64_t e = (int64_t)i * ld + p;
+      store_param(x, dtype, e, z[e]);
+      store_param(y, dtype, e, load_param(x, dtype, e));
+    }
+  return 0;
+}
+
+/* Local-DAdam (App. C): the outer optimizer is applied at the end of the
+ * local block with a DAdam-style disagreement of the pre-update parameters,
+ *   d_i = sum_j w_ij (x_i - x_j),  x_i <- OuterOpt(y_i, d_i).
+ * z: [n, ld] scratch. */
+int orc_local_dadam_round(int n, int64_t P, int64_t ld, int dtype, void *x, void *y, REAL *u, REAL *z,
+                          const int32_t *row_ptr, const int32_t *col, const REAL *val, double mu,
+                          double eta, int nesterov) {
+  if (n < 1 || P < 0 || ld < P || !dtype_ok(dtype) || !csr_ok(n, row_ptr, col)) return -1;
+  const REAL mur = (REAL)mu, etar = (REAL)eta;
+  for (int i = 0; i < n; ++i) {
+    for (int64_t p = 0; p < P; ++p) {
+      int64_t e = (int64_t)i * ld + p;
+      REAL xi = load_param(x, dtype, e);
+      REAL d = 0;
+      for (int32_t kk = row_ptr[i]; kk < row_ptr[i + 1]; ++kk)
+        d = d + val[kk] * (xi - load_param(x, dtype, (int64_t)col[kk] * ld + p));
+      z[e] = outer_step(load_param(y, dtype, e), d, &u[e], mur, etar, nesterov);
+    }
+  }
+  for (int i = 0; i < n; ++i)
+    for (int64_t p = 0; p < P; ++p) {
+      int64_t e = (int64_t)i * ld + p;
+      store_param(x, dtype, e, z[e]);
+      store_param(y, dtype, e, load_param(x, dtype, e));
+    }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Consensus error and network average.                                     */
 /* ------------------------------------------------------------------------ */
 

@@ -71,6 +71,14 @@ def _load(tag):
     lib.orc_gossip_round.restype = ctypes.c_int
     lib.orc_gossip_round.argtypes = [ctypes.c_int, _i64, _i64, ctypes.c_int, _vp, _vp, _vp, _vp, _vp,
                                      _vp, _vp, _vp, _d, _d, ctypes.c_int, _d, _i64]
+    lib.orc_alg1_round.restype = ctypes.c_int
+    lib.orc_alg1_round.argtypes = [ctypes.c_int, _i64, _i64, ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp,
+                                   _d, _d, ctypes.c_int]
+    lib.orc_dadam_round.restype = ctypes.c_int
+    lib.orc_dadam_round.argtypes = [ctypes.c_int, _i64, _i64, ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp]
+    lib.orc_local_dadam_round.restype = ctypes.c_int
+    lib.orc_local_dadam_round.argtypes = [ctypes.c_int, _i64, _i64, ctypes.c_int, _vp, _vp, _vp, _vp, _vp,
+                                          _vp, _vp, _d, _d, ctypes.c_int]
     lib.orc_consensus_error.restype = _d
     lib.orc_consensus_error.argtypes = [ctypes.c_int, _i64, _i64, ctypes.c_int, _vp]
     lib.orc_replica_mean.restype = None
@@ -180,6 +188,8 @@ class OracleHParams:
     outer_momentum: float = 0.9
     nesterov: bool = True
     consensus_momentum: float = 0.1
+    # "eq": Eq. 1 / Eq. 2; "alg1": Algorithm 1; "dadam", "local_dadam": App. C
+    form: str = "eq"
 
 
 class Oracle:
@@ -252,11 +262,20 @@ class Oracle:
         col = np.ascontiguousarray(col, dtype=np.int32)
         val = np.ascontiguousarray(val, dtype=self.real)
         hp = self.hp
-        rc = self.L.orc_gossip_round(self.n, self.P, self.P, self.pcode, _ptr(self.x), _ptr(self.y),
-                                     _ptr(self.u), _ptr(self.zp), _ptr(self.z), _ptr(row_ptr),
-                                     _ptr(col), _ptr(val), self._h(hp.outer_momentum),
-                                     self._h(hp.outer_lr), int(bool(hp.nesterov)),
-                                     self._h(hp.consensus_momentum), self.rounds_done)
+        common = (self.n, self.P, self.P, self.pcode, _ptr(self.x), _ptr(self.y))
+        outer = (self._h(hp.outer_momentum), self._h(hp.outer_lr), int(bool(hp.nesterov)))
+        csr = (_ptr(row_ptr), _ptr(col), _ptr(val))
+        if hp.form == "eq":
+            rc = self.L.orc_gossip_round(*common, _ptr(self.u), _ptr(self.zp), _ptr(self.z), *csr, *outer[:2],
+                                         outer[2], self._h(hp.consensus_momentum), self.rounds_done)
+        elif hp.form == "alg1":
+            rc = self.L.orc_alg1_round(*common, _ptr(self.u), *csr, *outer)
+        elif hp.form == "dadam":
+            rc = self.L.orc_dadam_round(*common, _ptr(self.z), *csr)
+        elif hp.form == "local_dadam":
+            rc = self.L.orc_local_dadam_round(*common, _ptr(self.u), _ptr(self.z), *csr, *outer)
+        else:
+            raise ValueError("unknown round form %r" % hp.form)
         if rc != 0:
             raise ValueError("oracle gossip_round rejected its arguments")
         self.rounds_done += 1
