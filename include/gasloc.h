@@ -82,6 +82,22 @@ typedef struct {
   uint64_t seed;
 } gasloc_topology;
 
+/* How a round combines the workers' local iterates (the CSR W as below):
+ *   EQ          z_i = x_i - eta (delta_i + mu u_i) with delta_i = x_i - y_i,
+ *               x_i <- sum_j W_ij z_j + gamma (z_i - zp_i)    (Eq. 1 and Eq. 2,
+ *               Nesterov outer step of section 4): the default
+ *   ALG1        x_i <- OuterOpt(x_i, sum_j W_ij (x_i - y_j))      (Algorithm 1)
+ *   DADAM       x_i <- sum_j W_ij x_j + (y_i - x_i)               (App. C)
+ *   LOCAL_DADAM x_i <- OuterOpt(y_i, sum_j W_ij (x_i - x_j))      (App. C)
+ * OuterOpt(b, d): u <- mu u + d; b - eta (d + mu u) (Nesterov) or b - eta u.
+ * Only EQ uses gamma; DADAM uses neither eta nor mu nor u. */
+typedef enum {
+  GASLOC_FORM_EQ = 0,
+  GASLOC_FORM_ALG1 = 1,
+  GASLOC_FORM_DADAM = 2,
+  GASLOC_FORM_LOCAL_DADAM = 3
+} gasloc_round_form;
+
 typedef struct {
   float beta1, beta2;          /* AdamW betas, 0 <= beta < 1 (paper: 0.9, 0.95)  */
   float eps;                   /* AdamW epsilon > 0 (added to sqrt(v_hat))       */
@@ -90,8 +106,10 @@ typedef struct {
   float outer_momentum;        /* mu in [0, 1); 0 gives Eq. 1's plain outer step   */
   int32_t outer_nesterov;      /* 1: Nesterov (z = x - eta (delta + mu u)),
                                   0: heavy ball (z = x - eta u)                   */
-  float consensus_momentum;    /* gamma in [0, 1) of Eq. 2; 0 disables zp         */
+  float consensus_momentum;    /* gamma in [0, 1) of Eq. 2; 0 disables zp; must be
+                                  0 unless round_form is EQ                       */
   int32_t param_dtype;         /* gasloc_dtype of x and y                          */
+  int32_t round_form;          /* gasloc_round_form                                */
 } gasloc_hparams;
 
 /* Caller-owned device buffers, row-major [n, ld] with row i at offset i*ld.
@@ -100,7 +118,8 @@ typedef struct {
  *   x  : round anchors x_t^i (param dtype)
  *   y  : live local iterates x_{t,h}^i (param dtype); see "deferred reset"
  *   m,v: AdamW moments (fp32)
- *   u  : outer momentum (fp32); may be NULL iff outer_momentum == 0
+ *   u  : outer momentum (fp32); may be NULL iff outer_momentum == 0 or the
+ *        form is DADAM
  *   zp : previous post-outer iterate x_{t-1} + eta g_{t-1} (fp32);
  *        may be NULL iff consensus_momentum == 0                              */
 typedef struct {
@@ -170,7 +189,8 @@ gasloc_status gasloc_gossip_round(gasloc_ctx *ctx, const gasloc_csr *W, uint64_t
  * x_{t+1}).  Use it for the last local step of a round (Algorithm 1: the
  * inner loop ends with y_i = x_i^{(t,H_i)}).  Saves 8 bytes per fp32
  * replica-parameter (12 when H_i = 1).  Same argument rules as the two calls;
- * enqueues two kernels and one CSR copy. */
+ * EINVAL for the DADAM and LOCAL_DADAM forms (use the two calls there).
+ * Enqueues two kernels and one CSR copy. */
 gasloc_status gasloc_local_step_gossip_round(gasloc_ctx *ctx, const float *grads, int64_t grad_ld,
                                              const uint8_t *active, float lr, const gasloc_csr *W,
                                              uint64_t t);

@@ -81,8 +81,8 @@ struct LaunchShape {
 
 // Launchers: enqueue on `stream`, return the launch status.
 hipError_t launch_local_adamw(const AdamArgs& a, int dtype, int blocks_per_worker, hipStream_t stream);
-hipError_t launch_gossip_round(const GossipArgs& a, int dtype, bool fused, const LaunchShape& shape,
-                               hipStream_t stream);
+hipError_t launch_gossip_round(const GossipArgs& a, int dtype, bool fused, int form,
+                               const LaunchShape& shape, hipStream_t stream);
 hipError_t launch_consensus_error(const void* x, int dtype, int64_t ld, int n, int64_t p_begin,
                                   int64_t p_end, double* partials, int blocks, hipStream_t stream);
 hipError_t launch_finalize(const double* partials, int count, double* out, hipStream_t stream);

@@ -246,10 +246,20 @@ __global__ __launch_bounds__(256) void k_local_adamw(AdamArgs a) {
 // a2-a5: pseudo-gradient, outer step, neighbour mix, consensus momentum and
 // the consensus-error partial, fused.  A thread owns V consecutive columns
 // of *every* worker, so each element of x, y, u, zp is read and written
-// exactly once and the in-place updates cannot race.  The post-outer
-// iterates z of all n workers at those columns sit in LDS (this thread's
-// private slots, so no barrier is needed between writing and gathering);
-// the CSR is staged in LDS once per workgroup.
+// exactly once and the in-place updates cannot race.  Phase 1 puts one value
+// per worker in this thread's private LDS slots (no barrier is needed
+// between writing and gathering them); phase 2 gathers the neighbours of
+// each row through the CSR, which is staged in LDS once per workgroup.
+//
+// What a slot holds and how a row is finished depends on the round form:
+//   EQ          slot z_j = x_j - eta (delta_j + mu u_j), delta_j = x_j - y_j
+//               x_i = sum_k W_ik z_k [+ gamma (z_i - zp_i)]      (Eq. 1, Eq. 2)
+//   ALG1        slot y_j;  delta_i = sum_k W_ik (x_i - y_k),
+//               x_i = OuterOpt(x_i, delta_i)                      (Algorithm 1)
+//   DADAM       slot x_j;  x_i = sum_k W_ik x_k + (y_i - x_i)     (App. C)
+//   LOCAL_DADAM slot x_j;  d_i = sum_k W_ik (x_i - x_k),
+//               x_i = OuterOpt(y_i, d_i)                          (App. C)
+// with OuterOpt(b, d): u = mu u + d; b - eta (d + mu u) (Nesterov) or b - eta u.
 // ---------------------------------------------------------------------------
 
 struct CsrEntry {
@@ -257,7 +267,14 @@ struct CsrEntry {
   float val;
 };
 
-template <int DT, int V, int R, bool FUSED>
+__device__ __forceinline__ float outer_step(float base, float d, float& u, float mu, float eta,
+                                            int nesterov) {
+  u = mu * u + d;
+  const float step = nesterov ? d + mu * u : u;
+  return base - eta * step;
+}
+
+template <int DT, int V, int R, bool FUSED, int FORM>
 __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int n = a.n;
@@ -274,6 +291,9 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
   for (int k = tid; k < nnz; k += nt) ent[k] = CsrEntry{a.col[k], a.val[k]};
   __syncthreads();
 
+  constexpr bool kEq = FORM == GASLOC_FORM_EQ;
+  constexpr bool kAlg1 = FORM == GASLOC_FORM_ALG1;
+  constexpr bool kMixesX = FORM == GASLOC_FORM_DADAM || FORM == GASLOC_FORM_LOCAL_DADAM;
   const double inv_n = 1.0 / static_cast<double>(n);
   const int64_t groups = (a.P + V - 1) / V;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * nt;
@@ -281,25 +301,29 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
   for (int64_t gi = static_cast<int64_t>(blockIdx.x) * nt + tid; gi < groups; gi += stride) {
     const int64_t p = gi * V;
     const int cnt = static_cast<int>(a.P - p < V ? a.P - p : V);
+    auto slot = [&](int j) { return zs + (static_cast<size_t>(j) * nt + tid) * V; };
 
-    // phase 1: [fused: last AdamW step ->] delta = x - y, outer (Nesterov /
-    // heavy-ball) step -> z.  The loads of R workers are issued together
-    // before any of them is used.
+    // phase 1: one slot value per worker; the loads of R workers are issued
+    // together before any of them is used
     for (int i0 = 0; i0 < n; i0 += R) {
       constexpr int RF = FUSED ? R : 1;
-      float xv[R][V], yv[R][V], uv[R][V];
+      constexpr int RU = kEq ? R : 1;
+      float xv[R][V], yv[R][V], uv[RU][V];
       float gv[RF][V], mv[RF][V], vv[RF][V];
 #pragma unroll
       for (int r = 0; r < R; ++r) {
         const int i = i0 + r;
         if (i >= n) break;
         const int64_t e = static_cast<int64_t>(i) * a.ld + p;
-        load_params<DT, V>(a.x, e, cnt, xv[r]);
-        if ((a.stepped >> i) & 1ull) {
-          load_params<DT, V>(a.y, e, cnt, yv[r]);
-        } else {
+        const bool stepped = (a.stepped >> i) & 1ull;
+        if (kEq || kMixesX || !stepped) load_params<DT, V>(a.x, e, cnt, xv[r]);
+        if constexpr (!kMixesX) {
+          if (stepped) {
+            load_params<DT, V>(a.y, e, cnt, yv[r]);
+          } else {
 #pragma unroll
-          for (int c = 0; c < V; ++c) yv[r][c] = xv[r][c];
+            for (int c = 0; c < V; ++c) yv[r][c] = xv[r][c];
+          }
         }
         if constexpr (FUSED) {
           if ((a.active >> i) & 1ull) {
@@ -308,11 +332,13 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
             load_f32<V>(a.v + e, cnt, vv[r]);
           }
         }
-        if (a.use_u) {
-          load_f32<V>(a.u + e, cnt, uv[r]);
-        } else {
+        if constexpr (kEq) {
+          if (a.use_u) {
+            load_f32<V>(a.u + e, cnt, uv[r]);
+          } else {
 #pragma unroll
-          for (int c = 0; c < V; ++c) uv[r][c] = 0.0f;
+            for (int c = 0; c < V; ++c) uv[r][c] = 0.0f;
+          }
         }
       }
 #pragma unroll
@@ -331,32 +357,55 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
             store_f32<V>(a.v + e, cnt, vv[r]);
           }
         }
-        float z[V];
+        float* out = slot(i);
+        if constexpr (kEq) {
 #pragma unroll
-        for (int c = 0; c < V; ++c) {
-          const float delta = xv[r][c] - yv[r][c];
-          uv[r][c] = a.mu * uv[r][c] + delta;
-          const float step = a.nesterov ? delta + a.mu * uv[r][c] : uv[r][c];
-          z[c] = xv[r][c] - a.eta * step;
+          for (int c = 0; c < V; ++c) out[c] = outer_step(xv[r][c], xv[r][c] - yv[r][c], uv[r][c], a.mu,
+                                                          a.eta, a.nesterov);
+          if (a.use_u) store_f32<V>(a.u + e, cnt, uv[r]);
+        } else if constexpr (kAlg1) {
+#pragma unroll
+          for (int c = 0; c < V; ++c) out[c] = yv[r][c];
+        } else {
+#pragma unroll
+          for (int c = 0; c < V; ++c) out[c] = xv[r][c];
         }
-        if (a.use_u) store_f32<V>(a.u + e, cnt, uv[r]);
-        float* zslot = zs + (static_cast<size_t>(i) * nt + tid) * V;
-#pragma unroll
-        for (int c = 0; c < V; ++c) zslot[c] = z[c];
       }
     }
 
-    // phase 2: x_i = sum_k W_ik z_k (+ gamma (z_i - zp_i)), zp_i = z_i,
-    // consensus error of the stored x from shifted fp64 sums
+    // phase 2: finish every row from the slots, store x (and u, zp), and
+    // accumulate the consensus error of the stored x from shifted fp64 sums
     double shift[V], s[V], q[V];
     for (int i0 = 0; i0 < n; i0 += R) {
-      float zpv[R][V];
-      if (a.apply_gamma) {
+      constexpr bool kRowX = kAlg1;                                  // x_i from HBM
+      constexpr bool kRowU = kAlg1 || FORM == GASLOC_FORM_LOCAL_DADAM;
+      constexpr bool kRowY = kMixesX;
+      float b0[R][V], b1v[(kRowU || kEq) ? R : 1][V];
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-          const int i = i0 + r;
-          if (i >= n) break;
-          load_f32<V>(a.zp + static_cast<int64_t>(i) * a.ld + p, cnt, zpv[r]);
+      for (int r = 0; r < R; ++r) {
+        const int i = i0 + r;
+        if (i >= n) break;
+        const int64_t e = static_cast<int64_t>(i) * a.ld + p;
+        if constexpr (kEq) {
+          if (a.apply_gamma) load_f32<V>(a.zp + e, cnt, b1v[r]);
+        }
+        if constexpr (kRowX) load_params<DT, V>(a.x, e, cnt, b0[r]);
+        if constexpr (kRowY) {
+          if ((a.stepped >> i) & 1ull) {
+            load_params<DT, V>(a.y, e, cnt, b0[r]);
+          } else {
+            const float* xi = slot(i);
+#pragma unroll
+            for (int c = 0; c < V; ++c) b0[r][c] = xi[c];
+          }
+        }
+        if constexpr (kRowU) {
+          if (a.use_u) {
+            load_f32<V>(a.u + e, cnt, b1v[r]);
+          } else {
+#pragma unroll
+            for (int c = 0; c < V; ++c) b1v[r][c] = 0.0f;
+          }
         }
       }
 #pragma unroll
@@ -364,27 +413,59 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
         const int i = i0 + r;
         if (i >= n) break;
         const int64_t e = static_cast<int64_t>(i) * a.ld + p;
-        float acc[V];
-#pragma unroll
-        for (int c = 0; c < V; ++c) acc[c] = 0.0f;
         const int kb = rp[i], ke = rp[i + 1];
-        for (int k = kb; k < ke; ++k) {
-          const CsrEntry w = ent[k];
-          const float* zj = zs + (static_cast<size_t>(w.col) * nt + tid) * V;
+        const float* own = slot(i);
+        float res[V];
+        if constexpr (kEq) {
 #pragma unroll
-          for (int c = 0; c < V; ++c) acc[c] = acc[c] + w.val * zj[c];
+          for (int c = 0; c < V; ++c) res[c] = 0.0f;
+          for (int k = kb; k < ke; ++k) {
+            const CsrEntry w = ent[k];
+            const float* zj = slot(w.col);
+#pragma unroll
+            for (int c = 0; c < V; ++c) res[c] = res[c] + w.val * zj[c];
+          }
+          float zcur[V];
+#pragma unroll
+          for (int c = 0; c < V; ++c) zcur[c] = own[c];
+          if (a.apply_gamma) {
+#pragma unroll
+            for (int c = 0; c < V; ++c) res[c] = res[c] + a.gamma * (zcur[c] - b1v[r][c]);
+          }
+          if (a.store_zp) store_f32<V>(a.zp + e, cnt, zcur);
+        } else if constexpr (FORM == GASLOC_FORM_DADAM) {
+#pragma unroll
+          for (int c = 0; c < V; ++c) res[c] = 0.0f;
+          for (int k = kb; k < ke; ++k) {
+            const CsrEntry w = ent[k];
+            const float* xj = slot(w.col);
+#pragma unroll
+            for (int c = 0; c < V; ++c) res[c] = res[c] + w.val * xj[c];
+          }
+#pragma unroll
+          for (int c = 0; c < V; ++c) res[c] = res[c] + (b0[r][c] - own[c]);
+        } else {
+          // ALG1: d = sum_k W_ik (x_i - y_k), base x_i;
+          // LOCAL_DADAM: d = sum_k W_ik (x_i - x_k), base y_i
+          float xi[V], d[V];
+#pragma unroll
+          for (int c = 0; c < V; ++c) {
+            xi[c] = kAlg1 ? b0[r][c] : own[c];
+            d[c] = 0.0f;
+          }
+          for (int k = kb; k < ke; ++k) {
+            const CsrEntry w = ent[k];
+            const float* oj = slot(w.col);
+#pragma unroll
+            for (int c = 0; c < V; ++c) d[c] = d[c] + w.val * (xi[c] - oj[c]);
+          }
+#pragma unroll
+          for (int c = 0; c < V; ++c)
+            res[c] = outer_step(kAlg1 ? xi[c] : b0[r][c], d[c], b1v[r][c], a.mu, a.eta, a.nesterov);
+          if (a.use_u) store_f32<V>(a.u + e, cnt, b1v[r]);
         }
-        const float* zi = zs + (static_cast<size_t>(i) * nt + tid) * V;
-        float zcur[V];
-#pragma unroll
-        for (int c = 0; c < V; ++c) zcur[c] = zi[c];
-        if (a.apply_gamma) {
-#pragma unroll
-          for (int c = 0; c < V; ++c) acc[c] = acc[c] + a.gamma * (zcur[c] - zpv[r][c]);
-        }
-        if (a.store_zp) store_f32<V>(a.zp + e, cnt, zcur);
         float kept[V];
-        store_params<DT, V>(a.x, e, cnt, acc, kept);
+        store_params<DT, V>(a.x, e, cnt, res, kept);
 #pragma unroll
         for (int c = 0; c < V; ++c) {
           const double xd = static_cast<double>(kept[c]);
@@ -393,9 +474,9 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
             s[c] = 0.0;
             q[c] = 0.0;
           }
-          const double d = xd - shift[c];
-          s[c] += d;
-          q[c] += d * d;
+          const double dv = xd - shift[c];
+          s[c] += dv;
+          q[c] += dv * dv;
         }
       }
     }
@@ -464,32 +545,52 @@ __global__ __launch_bounds__(256) void k_replica_mean(const void* x, int64_t ld,
   }
 }
 
-template <int DT, int V, int R, bool FUSED>
+template <int DT, int V, int R, bool FUSED, int FORM>
 hipError_t launch_gossip_typed(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
   const size_t lds = gossip_lds_bytes(a.n, a.nnz, s);
-  hipLaunchKernelGGL((k_gossip_round<DT, V, R, FUSED>), dim3(s.blocks), dim3(s.threads), lds, stream, a);
+  hipLaunchKernelGGL((k_gossip_round<DT, V, R, FUSED, FORM>), dim3(s.blocks), dim3(s.threads), lds, stream,
+                     a);
   return hipGetLastError();
 }
 
 // The fused kernel carries three more streams per worker, so it batches at
 // most 4 workers to stay within the register file.
-template <int DT, int V, bool FUSED>
+template <int DT, int V, bool FUSED, int FORM>
 hipError_t launch_gossip_batched(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
   switch (s.batch) {
-    case 1: return launch_gossip_typed<DT, V, 1, FUSED>(a, s, stream);
-    case 2: return launch_gossip_typed<DT, V, 2, FUSED>(a, s, stream);
+    case 1: return launch_gossip_typed<DT, V, 1, FUSED, FORM>(a, s, stream);
+    case 2: return launch_gossip_typed<DT, V, 2, FUSED, FORM>(a, s, stream);
     case 8:
-      if constexpr (!FUSED) return launch_gossip_typed<DT, V, 8, FUSED>(a, s, stream);
+      if constexpr (!FUSED) return launch_gossip_typed<DT, V, 8, FUSED, FORM>(a, s, stream);
       [[fallthrough]];
-    default: return launch_gossip_typed<DT, V, 4, FUSED>(a, s, stream);
+    default: return launch_gossip_typed<DT, V, 4, FUSED, FORM>(a, s, stream);
   }
 }
 
-template <int DT, bool FUSED>
-hipError_t launch_gossip_dtype(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
-  if (s.vec == 4) return launch_gossip_batched<DT, 4, FUSED>(a, s, stream);
-  if (s.vec == 2) return launch_gossip_batched<DT, 2, FUSED>(a, s, stream);
-  return launch_gossip_batched<DT, 1, FUSED>(a, s, stream);
+template <int DT, bool FUSED, int FORM>
+hipError_t launch_gossip_vec(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
+  if (s.vec == 4) return launch_gossip_batched<DT, 4, FUSED, FORM>(a, s, stream);
+  if (s.vec == 2) return launch_gossip_batched<DT, 2, FUSED, FORM>(a, s, stream);
+  return launch_gossip_batched<DT, 1, FUSED, FORM>(a, s, stream);
+}
+
+// The fused last local step exists for the forms whose slots hold the new
+// local iterate or depend on it in phase 1 (EQ, ALG1).
+template <int DT>
+hipError_t launch_gossip_dtype(const GossipArgs& a, bool fused, int form, const LaunchShape& s,
+                               hipStream_t stream) {
+  switch (form) {
+    case GASLOC_FORM_ALG1:
+      return fused ? launch_gossip_vec<DT, true, GASLOC_FORM_ALG1>(a, s, stream)
+                   : launch_gossip_vec<DT, false, GASLOC_FORM_ALG1>(a, s, stream);
+    case GASLOC_FORM_DADAM:
+      return launch_gossip_vec<DT, false, GASLOC_FORM_DADAM>(a, s, stream);
+    case GASLOC_FORM_LOCAL_DADAM:
+      return launch_gossip_vec<DT, false, GASLOC_FORM_LOCAL_DADAM>(a, s, stream);
+    default:
+      return fused ? launch_gossip_vec<DT, true, GASLOC_FORM_EQ>(a, s, stream)
+                   : launch_gossip_vec<DT, false, GASLOC_FORM_EQ>(a, s, stream);
+  }
 }
 
 }  // namespace
@@ -510,13 +611,10 @@ hipError_t launch_local_adamw(const AdamArgs& a, int dtype, int blocks_per_worke
   return hipGetLastError();
 }
 
-hipError_t launch_gossip_round(const GossipArgs& a, int dtype, bool fused, const LaunchShape& s,
+hipError_t launch_gossip_round(const GossipArgs& a, int dtype, bool fused, int form, const LaunchShape& s,
                                hipStream_t stream) {
-  if (dtype == GASLOC_BF16)
-    return fused ? launch_gossip_dtype<GASLOC_BF16, true>(a, s, stream)
-                 : launch_gossip_dtype<GASLOC_BF16, false>(a, s, stream);
-  return fused ? launch_gossip_dtype<GASLOC_F32, true>(a, s, stream)
-               : launch_gossip_dtype<GASLOC_F32, false>(a, s, stream);
+  if (dtype == GASLOC_BF16) return launch_gossip_dtype<GASLOC_BF16>(a, fused, form, s, stream);
+  return launch_gossip_dtype<GASLOC_F32>(a, fused, form, s, stream);
 }
 
 hipError_t launch_consensus_error(const void* x, int dtype, int64_t ld, int n, int64_t p_begin,

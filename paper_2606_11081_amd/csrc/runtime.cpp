@@ -135,6 +135,9 @@ std::string check_hparams(const gasloc_hparams& h) {
   if (!(finite(h.consensus_momentum) && h.consensus_momentum >= 0.0f && h.consensus_momentum < 1.0f))
     return "consensus_momentum must be in [0, 1)";
   if (h.param_dtype != GASLOC_F32 && h.param_dtype != GASLOC_BF16) return "param_dtype must be F32 or BF16";
+  if (h.round_form < GASLOC_FORM_EQ || h.round_form > GASLOC_FORM_LOCAL_DADAM) return "unknown round_form";
+  if (h.round_form != GASLOC_FORM_EQ && h.consensus_momentum != 0.0f)
+    return "consensus_momentum must be 0 unless round_form is EQ";
   return "";
 }
 
@@ -348,7 +351,7 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
   a.eta = c->hp.outer_lr;
   a.gamma = c->hp.consensus_momentum;
   a.nesterov = c->hp.outer_nesterov;
-  a.use_u = c->buf.u != nullptr;
+  a.use_u = c->buf.u != nullptr && c->hp.round_form != GASLOC_FORM_DADAM;
   a.store_zp = c->hp.consensus_momentum != 0.0f;
   a.apply_gamma = a.store_zp && c->rounds_done > 0;
   for (int i = 0; i < c->n; ++i)
@@ -369,7 +372,8 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
     std::memcpy(a.c2, step->c2, sizeof a.c2);
   }
   a.partials = c->d_partials;
-  HIP_TRY(c, gasloc::launch_gossip_round(a, c->hp.param_dtype, step != nullptr, shape, c->stream));
+  HIP_TRY(c, gasloc::launch_gossip_round(a, c->hp.param_dtype, step != nullptr, c->hp.round_form, shape,
+                                         c->stream));
   HIP_TRY(c, gasloc::launch_finalize(c->d_partials, shape.blocks, c->d_ce, c->stream));
   if (step) {
     for (int i = 0; i < c->n; ++i)
@@ -402,7 +406,7 @@ gasloc_status gasloc_init(int32_t n, int64_t P, const gasloc_topology* topology,
   if ((static_cast<uint64_t>(b.ld) * sp) % 16 != 0)
     return fail(nullptr, GASLOC_EINVAL, "ld * sizeof(param) must be a multiple of 16 bytes");
   if (!b.x || !b.y || !b.m || !b.v) return fail(nullptr, GASLOC_EINVAL, "x, y, m, v must not be NULL");
-  if (!b.u && hparams->outer_momentum != 0.0f)
+  if (!b.u && hparams->outer_momentum != 0.0f && hparams->round_form != GASLOC_FORM_DADAM)
     return fail(nullptr, GASLOC_EINVAL, "u may be NULL only when outer_momentum == 0");
   if (!b.zp && hparams->consensus_momentum != 0.0f)
     return fail(nullptr, GASLOC_EINVAL, "zp may be NULL only when consensus_momentum == 0");
@@ -548,6 +552,8 @@ gasloc_status gasloc_local_step_gossip_round(gasloc_ctx* c, const float* grads, 
                                              const uint8_t* active, float lr, const gasloc_csr* W, uint64_t t) {
   if (!c) return fail(nullptr, GASLOC_EINVAL, "NULL context");
   if (c->failed) return fail(c, GASLOC_ESTATE, "context unusable after a device error: " + c->err);
+  if (c->hp.round_form == GASLOC_FORM_DADAM || c->hp.round_form == GASLOC_FORM_LOCAL_DADAM)
+    return fail(c, GASLOC_EINVAL, "the fused last local step supports the EQ and ALG1 forms");
   gasloc_status st = check_step(c, grads, grad_ld, lr);
   if (st != GASLOC_OK) return st;
   const StepPlan plan = plan_step(*c, active, lr);

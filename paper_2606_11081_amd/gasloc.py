@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(_HERE, "libgasloc.so")
 GASLOC_OK, GASLOC_EINVAL, GASLOC_ENOMEM, GASLOC_EDEVICE, GASLOC_ESTATE = range(5)
 STATUS_NAMES = {0: "OK", 1: "EINVAL", 2: "ENOMEM", 3: "EDEVICE", 4: "ESTATE"}
 GASLOC_F32, GASLOC_BF16 = 0, 1
+ROUND_FORM = {"eq": 0, "alg1": 1, "dadam": 2, "local_dadam": 3}
 TOPOLOGY = {
     "explicit": 0,
     "ring": 1,
@@ -41,7 +42,8 @@ class gasloc_hparams(ctypes.Structure):
     _fields_ = [("beta1", ctypes.c_float), ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
                 ("weight_decay", ctypes.c_float), ("outer_lr", ctypes.c_float),
                 ("outer_momentum", ctypes.c_float), ("outer_nesterov", ctypes.c_int32),
-                ("consensus_momentum", ctypes.c_float), ("param_dtype", ctypes.c_int32)]
+                ("consensus_momentum", ctypes.c_float), ("param_dtype", ctypes.c_int32),
+                ("round_form", ctypes.c_int32)]
 
 
 class gasloc_buffers(ctypes.Structure):
@@ -122,10 +124,11 @@ def make_topology_struct(kind="ring", seed=0, degree=3):
 
 
 def make_hparams(beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1, outer_lr=0.7, outer_momentum=0.9,
-                 outer_nesterov=True, consensus_momentum=0.1, param_dtype="f32"):
+                 outer_nesterov=True, consensus_momentum=0.1, param_dtype="f32", round_form="eq"):
     dt = GASLOC_BF16 if param_dtype in ("bf16", GASLOC_BF16) else GASLOC_F32
+    form = ROUND_FORM[round_form] if isinstance(round_form, str) else int(round_form)
     return gasloc_hparams(beta1, beta2, eps, weight_decay, outer_lr, outer_momentum, int(bool(outer_nesterov)),
-                          consensus_momentum, dt)
+                          consensus_momentum, dt, form)
 
 
 def make_csr(row_ptr, col, val):
@@ -283,7 +286,8 @@ class GASLoC:
 
         self.n, self.P, self.param_dtype = int(n), int(P), param_dtype
         hpar = make_hparams(param_dtype=param_dtype, **hp)
-        self.bufs = alloc_buffers(n, P, param_dtype, device, with_u=hpar.outer_momentum != 0.0,
+        self.bufs = alloc_buffers(n, P, param_dtype, device,
+                                  with_u=hpar.outer_momentum != 0.0 and hpar.round_form != ROUND_FORM["dadam"],
                                   with_zp=hpar.consensus_momentum != 0.0)
         self.ld = self.bufs["ld"]
         self.stream = torch.cuda.current_stream(device) if stream is None else stream

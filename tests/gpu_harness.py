@@ -61,7 +61,7 @@ class Pair:
 
     def __init__(self, n, P, topology="ring", param_dtype="f32", gamma=0.1, mu=0.9, nesterov=True,
                  eta=0.7, seed=gi.SEED_TOPOLOGY, degree=3, cols=None, precisions=("f32", "f64"),
-                 lr=gi.LOCAL_LR):
+                 lr=gi.LOCAL_LR, form="eq"):
         import torch
 
         import paper_2606_11081_amd as g
@@ -71,13 +71,13 @@ class Pair:
         self.gpu = g.GASLoC(n, P, topology=topology, seed=seed, degree=degree, param_dtype=param_dtype,
                             beta1=gi.BETA1, beta2=gi.BETA2, eps=gi.EPS, weight_decay=gi.WEIGHT_DECAY,
                             outer_lr=eta, outer_momentum=mu, outer_nesterov=nesterov,
-                            consensus_momentum=gamma)
+                            consensus_momentum=gamma, round_form=form)
         self.cols = np.arange(P) if cols is None else np.asarray(cols)
         self.full = cols is None
         self.cols_dev = torch.as_tensor(self.cols, device="cuda")
         hp = oracle.OracleHParams(beta1=gi.BETA1, beta2=gi.BETA2, eps=gi.EPS, weight_decay=gi.WEIGHT_DECAY,
                                   outer_lr=eta, outer_momentum=mu, nesterov=nesterov,
-                                  consensus_momentum=gamma)
+                                  consensus_momentum=gamma, form=form)
         if param_dtype == "bf16":
             precisions = ("f32",)
         self.oracles = {p: oracle.Oracle(n, len(self.cols), hp, topology=topology, seed=seed, degree=degree,

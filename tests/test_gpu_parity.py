@@ -145,6 +145,66 @@ def test_fused_last_step_matches_two_calls_and_oracle(n, P, topology, dtype, H, 
     log("bit-exact fraction vs fp32 oracle: %s" % stats)
 
 
+FORMS = [
+    # form, n, P, topology, dtype, H, mu, nesterov
+    ("alg1", 8, 40_003, "exponential", "f32", 2, 0.9, True),
+    ("alg1", 16, 10_001, "one_peer_exp", "bf16", 1, 0.9, False),
+    ("alg1", 5, 777, "complete", "f32", 2, 0.0, True),
+    ("dadam", 8, 30_011, "two_peer", "f32", 1, 0.9, True),
+    ("dadam", 32, 4_099, "random_regular", "bf16", 2, 0.9, True),
+    ("local_dadam", 16, 20_000, "one_peer", "f32", 3, 0.9, True),
+    ("local_dadam", 7, 5_001, "ring", "bf16", 1, 0.5, False),
+    ("local_dadam", 64, 1_003, "one_peer", "f32", 2, 0.0, True),
+]
+
+
+@pytest.mark.parametrize("form,n,P,topology,dtype,H,mu,nesterov", FORMS)
+def test_round_forms(form, n, P, topology, dtype, H, mu, nesterov):
+    log("case form=%s n=%d P=%d %s %s H=%d mu=%g nesterov=%s" % (form, n, P, topology, dtype, H, mu, nesterov))
+    pair = Pair(n, P, topology, dtype, gamma=0.0, mu=mu, nesterov=nesterov, form=form)
+    H_i = np.full(n, H)
+    if n >= 5:
+        H_i[1] = 0
+    stats = _run(pair, 3, H_i, tag=form)
+    log("bit-exact fraction vs fp32 oracle: %s" % stats)
+    if form == "alg1" and topology == "complete":
+        x = pair.gather("x")
+        assert np.all(x == x[0]) and pair.gpu.consensus_error() == 0.0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_fused_last_step_alg1(dtype):
+    import torch
+
+    n, P = 8, 33_333
+    fused = Pair(n, P, "two_peer", dtype, gamma=0.0, form="alg1", precisions=("f32",))
+    split = Pair(n, P, "two_peer", dtype, gamma=0.0, form="alg1", precisions=())
+    for t in range(3):
+        for h in range(2):
+            split.local_step()
+            if h == 1:
+                fused.local_step_gossip_round(t)
+            else:
+                fused.local_step()
+        split.gossip_round(t)
+        assert fused.gpu.consensus_error() == split.gpu.consensus_error()
+    torch.cuda.synchronize()
+    for name in ("x", "m", "v", "u"):
+        assert torch.equal(getattr(fused.gpu, name)[:, :P], getattr(split.gpu, name)[:, :P]), name
+    fused.check_state(tag="fused alg1")
+
+
+def test_form_arguments_are_checked():
+    import paper_2606_11081_amd as g
+
+    with pytest.raises(g.GaslocError, match="consensus_momentum must be 0"):
+        g.GASLoC(4, 256, round_form="alg1", consensus_momentum=0.1)
+    d = g.GASLoC(4, 256, round_form="dadam", consensus_momentum=0.0)
+    grads = d.x.new_zeros((4, d.ld), dtype=d.m.dtype)
+    with pytest.raises(g.GaslocError, match="EQ and ALG1"):
+        d.local_step_gossip_round(grads, 0.01, 0)
+
+
 def test_explicit_nonsymmetric_csr_and_identity():
     n, P = 6, 5003
     rng = np.random.default_rng(3)
