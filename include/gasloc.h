@@ -223,6 +223,15 @@ gasloc_status gasloc_make_topology(const gasloc_topology *topology, int32_t n, u
                                    int32_t *row_ptr, int32_t *col, float *val, int32_t cap,
                                    int32_t *nnz);
 
+/* Local learning rate of step `step` (0-based, clamped to [0, total_steps])
+ * under the schedule of App. B "Optimization": a linear warmup over the first
+ * floor(warmup_frac * total_steps) steps from start_frac * peak to peak, then
+ * a half-cosine decay to final_frac * peak at total_steps.  The paper's
+ * setting is warmup_frac = 0.1, start_frac = 0.01 (final_frac unstated; 0 is
+ * the usual choice).  Evaluated in fp64, returned in fp32.  Host only. */
+float gasloc_lr_schedule(float peak, int64_t step, int64_t total_steps, float warmup_frac,
+                         float start_frac, float final_frac);
+
 /* Host-only CSR check with the rules listed at gasloc_csr (n must match). */
 gasloc_status gasloc_validate_csr(const gasloc_csr *W, int32_t n);
 

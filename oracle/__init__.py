@@ -13,6 +13,7 @@ from .oracle import (  # noqa: F401
     csr_to_dense,
     f32_to_bf16_bits,
     lib,
+    lr_schedule,
     round_state,
     shuffled_identity,
     splitmix64_stream,

@@ -366,6 +366,32 @@ int orc_local_step(int n, int64_t P, int64_t ld, int dtype, void *y, const float
   return 0;
 }
 
+/* Learning-rate schedule of App. B "Optimization": a warmup over the first
+ * warmup_frac of the steps that starts at start_frac of the peak, then
+ * cosine decay to final_frac of the peak at the last step.  Linear warmup and
+ * a half-cosine are the readings taken for the shapes the paper names.
+ *   s < W:  peak * (start + (1 - start) * s / W)
+ *   s >= W: peak * (final + (1 - final) * (1 + cos(pi * (s - W) / (T - W))) / 2)
+ * with W = floor(warmup_frac * T); evaluated in fp64, returned in fp32. */
+float orc_lr_schedule(double peak, int64_t step, int64_t total, double warmup_frac, double start_frac,
+                      double final_frac) {
+  if (total < 1) return (float)peak;
+  if (step < 0) step = 0;
+  if (step > total) step = total;
+  int64_t W = (int64_t)floor(warmup_frac * (double)total);
+  double lr;
+  if (step < W) {
+    lr = peak * (start_frac + (1.0 - start_frac) * (double)step / (double)W);
+  } else if (total == W) {
+    lr = peak;
+  } else {
+    double progress = (double)(step - W) / (double)(total - W);
+    double cosine = (1.0 + cos(3.14159265358979323846 * progress)) / 2.0;
+    lr = peak * (final_frac + (1.0 - final_frac) * cosine);
+  }
+  return (float)lr;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Outer step, mixing and consensus momentum (Eq. 1 outer loop, Eq. 2).    */
 /* ------------------------------------------------------------------------ */

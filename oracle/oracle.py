@@ -79,6 +79,8 @@ def _load(tag):
     lib.orc_local_dadam_round.restype = ctypes.c_int
     lib.orc_local_dadam_round.argtypes = [ctypes.c_int, _i64, _i64, ctypes.c_int, _vp, _vp, _vp, _vp, _vp,
                                           _vp, _vp, _d, _d, ctypes.c_int]
+    lib.orc_lr_schedule.restype = ctypes.c_float
+    lib.orc_lr_schedule.argtypes = [_d, _i64, _i64, _d, _d, _d]
     lib.orc_consensus_error.restype = _d
     lib.orc_consensus_error.argtypes = [ctypes.c_int, _i64, _i64, ctypes.c_int, _vp]
     lib.orc_replica_mean.restype = None
@@ -154,6 +156,10 @@ def csr_to_dense(row_ptr, col, val, n):
         for k in range(row_ptr[i], row_ptr[i + 1]):
             W[i, col[k]] = val[k]
     return W
+
+
+def lr_schedule(peak, step, total, warmup_frac=0.1, start_frac=0.01, final_frac=0.0):
+    return lib().orc_lr_schedule(peak, step, total, warmup_frac, start_frac, final_frac)
 
 
 def adamw_scalars(lr, beta1, beta2, wd, k, precision="f32"):

@@ -76,6 +76,8 @@ _SIGNATURES = {
     "gasloc_validate_csr": (ctypes.c_int, [ctypes.POINTER(gasloc_csr), _i32]),
     "gasloc_get_counters": (ctypes.c_int, [_vp, _vp, _vp, ctypes.POINTER(_i64)]),
     "gasloc_set_counters": (ctypes.c_int, [_vp, _vp, _vp, _i64]),
+    "gasloc_lr_schedule": (ctypes.c_float, [ctypes.c_float, _i64, _i64, ctypes.c_float, ctypes.c_float,
+                                            ctypes.c_float]),
     "gasloc_last_error": (ctypes.c_char_p, [_vp]),
     "gasloc_destroy": (None, [_vp]),
 }
@@ -242,6 +244,10 @@ def gasloc_set_counters(ctx, k, stepped, rounds_done):
     ss, sp = _host(stepped, np.uint8)
     _check(library().gasloc_set_counters(ctx, kp, sp, int(rounds_done)), ctx)
     del kk, ss
+
+
+def gasloc_lr_schedule(peak, step, total_steps, warmup_frac=0.1, start_frac=0.01, final_frac=0.0):
+    return library().gasloc_lr_schedule(peak, int(step), int(total_steps), warmup_frac, start_frac, final_frac)
 
 
 def gasloc_last_error(ctx=None):

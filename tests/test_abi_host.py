@@ -183,3 +183,16 @@ def test_null_context_is_rejected():
     out = ctypes.c_double()
     assert lib.gasloc_consensus_error(None, ctypes.byref(out)) == g.GASLOC_EINVAL
     lib.gasloc_destroy(None)  # ignored
+
+
+@pytest.mark.parametrize("total", [1, 9, 10, 100, 1000, 2569, 100_000])
+@pytest.mark.parametrize("fracs", [(0.1, 0.01, 0.0), (0.05, 0.1, 0.1), (0.0, 0.01, 0.0), (1.0, 0.01, 0.0)])
+def test_lr_schedule_bit_exact_with_oracle(total, fracs):
+    f32 = lambda v: float(np.float32(v))  # noqa: E731
+    peak = f32(4e-3)
+    w, s, f = (f32(v) for v in fracs)
+    steps = sorted(set(list(range(0, min(total, 300) + 1)) + [total // 2, total - 1, total, total + 3, -1]))
+    for step in steps:
+        got = g.gasloc_lr_schedule(peak, step, total, w, s, f)
+        exp = oracle.lr_schedule(peak, step, total, w, s, f)
+        assert np.float32(got).view(np.uint32) == np.float32(exp).view(np.uint32), (step, got, exp)
