@@ -16,6 +16,7 @@ from .oracle import (  # noqa: F401
     lr_schedule,
     round_state,
     shuffled_identity,
+    skip_exchanges,
     splitmix64_stream,
     topology_csr,
 )

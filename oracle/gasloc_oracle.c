@@ -198,8 +198,47 @@ static int random_regular_adj(int n, int d, uint64_t *state, unsigned char *adj)
 /* Build the mixing matrix of round t into the CSR arrays.  Returns nnz, or
  * -1 on bad arguments / overflow of cap.  `degree` is used by the random
  * regular graph only. */
+/* Metropolis-Hastings weights on the graph in adj (self loops ignored):
+ * W_ij = 1/(1 + max(d_i, d_j)) for every edge, W_ii = 1 - sum_j W_ij. */
+static void metropolis_rows(int n, unsigned char *adj, double *W) {
+  int deg[ORC_MAX_N];
+  for (int i = 0; i < n; ++i) {
+    deg[i] = 0;
+    for (int j = 0; j < n; ++j) deg[i] += (j != i && adj[i * n + j]);
+  }
+  for (int i = 0; i < n; ++i) {
+    double off = 0.0;
+    for (int j = 0; j < n; ++j) {
+      W[i * n + j] = 0.0;
+      if (j == i || !adj[i * n + j]) continue;
+      int dmax = deg[i] > deg[j] ? deg[i] : deg[j];
+      W[i * n + j] = 1.0 / (1.0 + (double)dmax);
+      off += W[i * n + j];
+    }
+    W[i * n + i] = 1.0 - off;
+    adj[i * n + i] = 1;
+  }
+}
+
+/* As orc_topology, with the randomized 1-Peer and 2-Peer selections
+ * restricted to the edges of an admissible graph (App. B.1: restrict the
+ * possible peer selections to the edges of the underlying graph).
+ * admissible: n*n row-major 0/1, symmetric; NULL means the complete graph.
+ * A restricted draw keeps a selected pair only if it is admissible, and its
+ * weights are Metropolis-Hastings (equal to the uniform 1/2 and 1/3 of the
+ * unrestricted draws, and doubly stochastic for any degrees). */
+int orc_topology_restricted(int kind, int n, int degree, uint64_t seed, uint64_t t,
+                            const unsigned char *admissible, int32_t *row_ptr, int32_t *col, REAL *val,
+                            int cap);
+
 int orc_topology(int kind, int n, int degree, uint64_t seed, uint64_t t, int32_t *row_ptr,
                  int32_t *col, REAL *val, int cap) {
+  return orc_topology_restricted(kind, n, degree, seed, t, NULL, row_ptr, col, val, cap);
+}
+
+int orc_topology_restricted(int kind, int n, int degree, uint64_t seed, uint64_t t,
+                            const unsigned char *admissible, int32_t *row_ptr, int32_t *col, REAL *val,
+                            int cap) {
   if (n < 1 || n > ORC_MAX_N) return -1;
   unsigned char *adj = (unsigned char *)calloc((size_t)n * (size_t)n, 1);
   double *W = (double *)calloc((size_t)n * (size_t)n, sizeof(double));
@@ -213,6 +252,7 @@ int orc_topology(int kind, int n, int degree, uint64_t seed, uint64_t t, int32_t
   int ok = 1;
   uint64_t state = orc_round_state(seed, t);
   for (int i = 0; i < n; ++i) sigma[i] = i;
+  if (admissible && kind != ORC_TOPO_ONE_PEER && kind != ORC_TOPO_TWO_PEER) ok = 0;
 
   if (kind == ORC_TOPO_RING) {
     /* static cycle i-1, i, i+1 (Tables 1-3, "ring") */
@@ -249,10 +289,14 @@ int orc_topology(int kind, int n, int degree, uint64_t seed, uint64_t t, int32_t
     for (int i = 0; i < n; ++i) adj[i * n + i] = 1;
     for (int k = 0; 2 * k + 1 < n; ++k) {
       int a = sigma[2 * k], b = sigma[2 * k + 1];
+      if (admissible && !admissible[a * n + b]) continue;
       adj[a * n + b] = 1;
       adj[b * n + a] = 1;
     }
-    uniform_rows(n, adj, W);
+    if (admissible)
+      metropolis_rows(n, adj, W);
+    else
+      uniform_rows(n, adj, W);
   } else if (kind == ORC_TOPO_TWO_PEER) {
     /* randomized 2-Peer (section 3.2): the permutation read as a cycle, each
      * node linked with both cyclic neighbours (symmetrised). */
@@ -260,10 +304,14 @@ int orc_topology(int kind, int n, int degree, uint64_t seed, uint64_t t, int32_t
     for (int i = 0; i < n; ++i) adj[i * n + i] = 1;
     for (int k = 0; k < n; ++k) {
       int a = sigma[k], b = sigma[(k + 1) % n];
+      if (admissible && !admissible[a * n + b]) continue;
       adj[a * n + b] = 1;
       adj[b * n + a] = 1;
     }
-    uniform_rows(n, adj, W);
+    if (admissible)
+      metropolis_rows(n, adj, W);
+    else
+      uniform_rows(n, adj, W);
   } else if (kind == ORC_TOPO_RANDOM_REGULAR) {
     /* a fresh random d-regular graph each round, Metropolis-Hastings weights
      * W_ij = 1/(1 + max(deg_i, deg_j)), W_ii = 1 - sum_j W_ij */
@@ -313,6 +361,65 @@ int orc_topology(int kind, int n, int degree, uint64_t seed, uint64_t t, int32_t
   free(adj);
   free(W);
   free(sigma);
+  return ok ? nnz : -1;
+}
+
+/* Fault tolerance (section 3.2, "Fault tolerance": failed exchanges can be
+ * skipped).  An exchange {i, j}, i != j, is skipped when worker i or j is
+ * dead (alive[.] == 0) or the link failed (link_ok[i*n+j] == 0 or
+ * link_ok[j*n+i] == 0); each endpoint then keeps for itself the weight it
+ * would have given the other: W_ii += W_ij, W_ij = 0.  alive / link_ok may be
+ * NULL (all alive / all links up).  The new diagonal is summed in fp64 in
+ * ascending column order and rounded once.  Returns the new nnz or -1. */
+int orc_skip_exchanges(int n, const int32_t *row_ptr, const int32_t *col, const REAL *val,
+                       const unsigned char *alive, const unsigned char *link_ok, int32_t *out_row_ptr,
+                       int32_t *out_col, REAL *out_val, int cap) {
+  if (n < 1 || n > ORC_MAX_N) return -1;
+  double *W = (double *)calloc((size_t)n * (size_t)n, sizeof(double));
+  unsigned char *nz = (unsigned char *)calloc((size_t)n * (size_t)n, 1);
+  if (!W || !nz) {
+    free(W);
+    free(nz);
+    return -1;
+  }
+  for (int i = 0; i < n; ++i)
+    for (int32_t k = row_ptr[i]; k < row_ptr[i + 1]; ++k) {
+      W[i * n + col[k]] = (double)val[k];
+      nz[i * n + col[k]] = 1;
+    }
+  for (int i = 0; i < n; ++i) {
+    double diag = W[i * n + i];
+    for (int j = 0; j < n; ++j) {
+      if (j == i || !nz[i * n + j]) continue;
+      int skip = (alive && (!alive[i] || !alive[j])) ||
+                 (link_ok && (!link_ok[i * n + j] || !link_ok[j * n + i]));
+      if (!skip) continue;
+      diag += W[i * n + j];
+      W[i * n + j] = 0.0;
+      nz[i * n + j] = 0;
+    }
+    if (diag != W[i * n + i] || nz[i * n + i]) {
+      W[i * n + i] = diag;
+      nz[i * n + i] = 1;
+    }
+  }
+  int nnz = 0, ok = 1;
+  out_row_ptr[0] = 0;
+  for (int i = 0; i < n && ok; ++i) {
+    for (int j = 0; j < n; ++j) {
+      if (!nz[i * n + j]) continue;
+      if (nnz >= cap) {
+        ok = 0;
+        break;
+      }
+      out_col[nnz] = j;
+      out_val[nnz] = (REAL)W[i * n + j];
+      ++nnz;
+    }
+    out_row_ptr[i + 1] = nnz;
+  }
+  free(W);
+  free(nz);
   return ok ? nnz : -1;
 }
 

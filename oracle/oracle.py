@@ -63,6 +63,11 @@ def _load(tag):
     lib.orc_topology.restype = ctypes.c_int
     lib.orc_topology.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_uint64,
                                  ctypes.c_uint64, _vp, _vp, _vp, ctypes.c_int]
+    lib.orc_topology_restricted.restype = ctypes.c_int
+    lib.orc_topology_restricted.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_uint64,
+                                            ctypes.c_uint64, _vp, _vp, _vp, _vp, ctypes.c_int]
+    lib.orc_skip_exchanges.restype = ctypes.c_int
+    lib.orc_skip_exchanges.argtypes = [ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_int]
     lib.orc_adamw_scalars.restype = None
     lib.orc_adamw_scalars.argtypes = [_d, _d, _d, _d, _i64, _vp, _vp, _vp]
     lib.orc_local_step.restype = ctypes.c_int
@@ -133,21 +138,45 @@ def shuffled_identity(state, N):
     return a
 
 
-def topology_csr(kind, n, seed, t, degree=3, precision="f32"):
+def topology_csr(kind, n, seed, t, degree=3, precision="f32", admissible=None):
     """CSR (row_ptr int32[n+1], col int32[nnz], val[nnz]) of round t.
 
     Weights are float32 from the fp32 oracle (the library's CSR format) and
-    float64 from the fp64 oracle.
+    float64 from the fp64 oracle.  admissible: optional [n, n] 0/1 matrix
+    restricting the randomized 1-/2-Peer selections.
     """
     cap = n * n
     row_ptr = np.zeros(n + 1, dtype=np.int32)
     col = np.zeros(max(cap, 1), dtype=np.int32)
     val = np.zeros(max(cap, 1), dtype=np.float32 if precision == "f32" else np.float64)
-    nnz = lib(precision).orc_topology(TOPOLOGY_CODES[kind], n, degree, seed, t, _ptr(row_ptr), _ptr(col),
-                             _ptr(val), cap)
+    adm = None if admissible is None else np.ascontiguousarray(admissible, dtype=np.uint8)
+    nnz = lib(precision).orc_topology_restricted(TOPOLOGY_CODES[kind], n, degree, seed, t,
+                                                 None if adm is None else _ptr(adm), _ptr(row_ptr),
+                                                 _ptr(col), _ptr(val), cap)
     if nnz < 0:
         raise ValueError("oracle: bad topology arguments (%s, n=%d, degree=%d)" % (kind, n, degree))
     return row_ptr, col[:nnz].copy(), val[:nnz].copy()
+
+
+def skip_exchanges(W, n, alive=None, link_ok=None, precision="f32"):
+    """The CSR W with every exchange of a dead worker or a failed link skipped."""
+    rp, col, val = W
+    real = np.float32 if precision == "f32" else np.float64
+    rp = np.ascontiguousarray(rp, dtype=np.int32)
+    col = np.ascontiguousarray(col, dtype=np.int32)
+    val = np.ascontiguousarray(val, dtype=real)
+    al = None if alive is None else np.ascontiguousarray(alive, dtype=np.uint8)
+    lk = None if link_ok is None else np.ascontiguousarray(link_ok, dtype=np.uint8)
+    cap = n * n
+    orp = np.zeros(n + 1, np.int32)
+    ocol = np.zeros(cap, np.int32)
+    oval = np.zeros(cap, real)
+    nnz = lib(precision).orc_skip_exchanges(n, _ptr(rp), _ptr(col), _ptr(val), None if al is None else _ptr(al),
+                                            None if lk is None else _ptr(lk), _ptr(orp), _ptr(ocol), _ptr(oval),
+                                            cap)
+    if nnz < 0:
+        raise ValueError("oracle: bad skip_exchanges arguments")
+    return orp, ocol[:nnz].copy(), oval[:nnz].copy()
 
 
 def csr_to_dense(row_ptr, col, val, n):
@@ -202,8 +231,9 @@ class Oracle:
     """All n workers' state on the host; P columns (or a sample of columns)."""
 
     def __init__(self, n, P, hp, topology="ring", seed=0, degree=3, precision="f32",
-                 param_dtype="f32"):
+                 param_dtype="f32", admissible=None):
         self.n, self.P, self.hp = int(n), int(P), hp
+        self.admissible = admissible
         self.topology, self.seed, self.degree = topology, int(seed), int(degree)
         self.precision = precision
         self.L = lib(precision)
@@ -260,7 +290,7 @@ class Oracle:
             raise ValueError("oracle local_step rejected its arguments")
 
     def csr(self, t):
-        return topology_csr(self.topology, self.n, self.seed, t, self.degree, self.precision)
+        return topology_csr(self.topology, self.n, self.seed, t, self.degree, self.precision, self.admissible)
 
     def gossip_round(self, t=0, csr=None):
         row_ptr, col, val = self.csr(t) if csr is None else csr
