@@ -80,6 +80,12 @@ typedef struct {
   int32_t kind;   /* gasloc_topology_kind                                        */
   int32_t degree; /* GASLOC_TOPO_RANDOM_REGULAR only: 0 <= degree < n, n*degree even */
   uint64_t seed;
+  /* Optional (NULL = complete graph): host uint8 [n*n] row-major, symmetric,
+   * 1 where an exchange is possible.  Restricts the ONE_PEER / TWO_PEER
+   * selections to these edges (App. B.1); the weights are then
+   * Metropolis-Hastings, which equal 1/2 and 1/3 when nothing is removed.
+   * gasloc_init copies it. */
+  const uint8_t *admissible;
 } gasloc_topology;
 
 /* How a round combines the workers' local iterates (the CSR W as below):
@@ -231,6 +237,23 @@ gasloc_status gasloc_make_topology(const gasloc_topology *topology, int32_t n, u
  * the usual choice).  Evaluated in fp64, returned in fp32.  Host only. */
 float gasloc_lr_schedule(float peak, int64_t step, int64_t total_steps, float warmup_frac,
                          float start_frac, float final_frac);
+
+/* Skipped exchanges (section 3.2, "Fault tolerance"), host only: W with
+ * every exchange {i, j} removed whose worker i or j is dead (alive[.] == 0)
+ * or whose link failed (link_ok[i*n + j] == 0 or link_ok[j*n + i] == 0);
+ * each worker keeps the weight it would have given the other (W_ii += W_ij),
+ * so rows still sum to 1 and a symmetric W stays doubly stochastic.  alive:
+ * uint8[n] or NULL (all alive); link_ok: uint8[n*n] or NULL (all up).  Output
+ * arrays as for gasloc_make_topology. */
+gasloc_status gasloc_skip_exchanges(const gasloc_csr *W, const uint8_t *alive, const uint8_t *link_ok,
+                                    int32_t *row_ptr, int32_t *col, float *val, int32_t cap,
+                                    int32_t *nnz);
+
+/* Marks workers dead or alive on a context (alive: host uint8[n]; NULL = all
+ * alive).  From the next call on, the exchanges of dead workers are skipped
+ * in every round's W (generated or passed in), as gasloc_skip_exchanges
+ * does, and dead workers take no local steps whatever `active` says. */
+gasloc_status gasloc_set_alive(gasloc_ctx *ctx, const uint8_t *alive);
 
 /* Host-only CSR check with the rules listed at gasloc_csr (n must match). */
 gasloc_status gasloc_validate_csr(const gasloc_csr *W, int32_t n);

@@ -15,6 +15,9 @@ constexpr int kMaxReplicas = 64;
 
 bool make_topology(const gasloc_topology& topo, int n, uint64_t t, int32_t* row_ptr, int32_t* col,
                    float* val, int32_t cap, int32_t* nnz, std::string* err);
+bool skip_exchanges(int n, const int32_t* rp, const int32_t* col, const float* val, const uint8_t* alive,
+                    const uint8_t* link_ok, int32_t* out_rp, int32_t* out_col, float* out_val, int32_t cap,
+                    int32_t* nnz, std::string* err);
 
 // ---------------------------------------------------------------------------
 // kernel arguments (passed by value)

@@ -55,6 +55,11 @@ struct gasloc_ctx {
   int device = 0;
   int cus = 0;
 
+  std::vector<uint8_t> admissible;  // copy of the topology's admissible graph (or empty)
+  std::vector<uint8_t> alive;       // 1 per live worker
+  bool any_dead = false;
+  std::vector<int32_t> skip_rp, skip_col;  // scratch for skipped exchanges
+  std::vector<float> skip_val;
   std::vector<int64_t> k;         // AdamW step count per worker
   std::vector<uint8_t> stepped;   // local steps taken since the last round
   int64_t rounds_done = 0;
@@ -279,7 +284,7 @@ StepPlan plan_step(const gasloc_ctx& c, const uint8_t* active, float lr) {
   s.omb2 = static_cast<float>(1.0 - b2);
   s.eps = c.hp.eps;
   for (int i = 0; i < c.n; ++i) {
-    if (active && !active[i]) continue;
+    if ((active && !active[i]) || !c.alive[static_cast<size_t>(i)]) continue;
     const double k = static_cast<double>(c.k[static_cast<size_t>(i)] + 1);
     s.s1[i] = static_cast<float>(lr64 / (1.0 - std::pow(b1, k)));
     s.c2[i] = static_cast<float>(std::sqrt(1.0 - std::pow(b2, k)));
@@ -321,6 +326,15 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
     rp = c->row_ptr.data();
     col = c->col.data();
     val = c->val.data();
+  }
+  if (c->any_dead) {
+    std::string err;
+    if (!gasloc::skip_exchanges(c->n, rp, col, val, c->alive.data(), nullptr, c->skip_rp.data(),
+                                c->skip_col.data(), c->skip_val.data(), c->n * c->n, &nnz, &err))
+      return fail(c, GASLOC_EINVAL, "skipping exchanges: " + err);
+    rp = c->skip_rp.data();
+    col = c->skip_col.data();
+    val = c->skip_val.data();
   }
   DeviceGuard guard(c->device);
   gasloc::LaunchShape shape = pick_gossip_shape(*c, nnz);
@@ -426,6 +440,20 @@ gasloc_status gasloc_init(int32_t n, int64_t P, const gasloc_topology* topology,
   c->stream = static_cast<hipStream_t>(hip_stream);
   c->k.assign(static_cast<size_t>(n), 0);
   c->stepped.assign(static_cast<size_t>(n), 0);
+  c->alive.assign(static_cast<size_t>(n), 1);
+  if (topology->admissible) {
+    c->admissible.assign(topology->admissible, topology->admissible + static_cast<size_t>(n) * n);
+    for (int i = 0; i < n; ++i)
+      for (int j = 0; j < n; ++j)
+        if ((c->admissible[static_cast<size_t>(i) * n + j] != 0) != (c->admissible[static_cast<size_t>(j) * n + i] != 0)) {
+          delete c;
+          return fail(nullptr, GASLOC_EINVAL, "the admissible graph must be symmetric");
+        }
+    c->topo.admissible = c->admissible.data();
+  }
+  c->skip_rp.resize(static_cast<size_t>(n) + 1);
+  c->skip_col.resize(static_cast<size_t>(n) * n);
+  c->skip_val.resize(static_cast<size_t>(n) * n);
   c->row_ptr.resize(static_cast<size_t>(n) + 1);
   c->col.resize(static_cast<size_t>(n) * n);
   c->val.resize(static_cast<size_t>(n) * n);
@@ -611,6 +639,29 @@ gasloc_status gasloc_make_topology(const gasloc_topology* topology, int32_t n, u
   std::string err;
   if (!gasloc::make_topology(*topology, n, t, row_ptr, col, val, cap, nnz, &err))
     return fail(nullptr, GASLOC_EINVAL, "topology: " + err);
+  return GASLOC_OK;
+}
+
+gasloc_status gasloc_skip_exchanges(const gasloc_csr* W, const uint8_t* alive, const uint8_t* link_ok,
+                                    int32_t* row_ptr, int32_t* col, float* val, int32_t cap, int32_t* nnz) {
+  if (!W || !row_ptr || !col || !val || !nnz) return fail(nullptr, GASLOC_EINVAL, "NULL argument");
+  if (W->n < 1 || W->n > kMaxReplicas) return fail(nullptr, GASLOC_EINVAL, "n outside [1, 64]");
+  const std::string e = check_csr(*W, W->n);
+  if (!e.empty()) return fail(nullptr, GASLOC_EINVAL, e);
+  std::string err;
+  if (!gasloc::skip_exchanges(W->n, W->row_ptr, W->col, W->val, alive, link_ok, row_ptr, col, val, cap, nnz,
+                              &err))
+    return fail(nullptr, GASLOC_EINVAL, err);
+  return GASLOC_OK;
+}
+
+gasloc_status gasloc_set_alive(gasloc_ctx* c, const uint8_t* alive) {
+  if (!c) return fail(nullptr, GASLOC_EINVAL, "NULL context");
+  c->any_dead = false;
+  for (int i = 0; i < c->n; ++i) {
+    c->alive[static_cast<size_t>(i)] = alive ? (alive[i] ? 1 : 0) : 1;
+    if (!c->alive[static_cast<size_t>(i)]) c->any_dead = true;
+  }
   return GASLOC_OK;
 }
 

@@ -106,6 +106,39 @@ bool emit_uniform(const Neighbours& nb, int32_t* row_ptr, int32_t* col, float* v
   return true;
 }
 
+// Emits the CSR with Metropolis-Hastings weights on the neighbour sets:
+// 1/(1 + max(d_i, d_j)) off the diagonal (d = neighbours other than self),
+// the rest of the row on the diagonal; doubly stochastic for any degrees.
+bool emit_metropolis(const Neighbours& nb, int32_t* row_ptr, int32_t* col, float* val, int32_t cap,
+                     int32_t* nnz, std::string* err) {
+  const int n = static_cast<int>(nb.size());
+  int32_t k = 0;
+  row_ptr[0] = 0;
+  for (int i = 0; i < n; ++i) {
+    const auto& row = nb[static_cast<size_t>(i)];
+    const int di = static_cast<int>(row.size()) - 1;
+    auto weight = [&](int j) {
+      const int dj = static_cast<int>(nb[static_cast<size_t>(j)].size()) - 1;
+      return 1.0 / (1.0 + static_cast<double>(std::max(di, dj)));
+    };
+    double off_sum = 0.0;
+    for (int j : row)
+      if (j != i) off_sum += weight(j);
+    for (int j : row) {
+      if (k >= cap) {
+        *err = "CSR capacity " + std::to_string(cap) + " too small";
+        return false;
+      }
+      col[k] = j;
+      val[k] = static_cast<float>(j == i ? 1.0 - off_sum : weight(j));
+      ++k;
+    }
+    row_ptr[i + 1] = k;
+  }
+  *nnz = k;
+  return true;
+}
+
 // Random `deg`-regular simple graph: deg*n half-edge points, point q is
 // owned by worker q / deg; shuffle, pair consecutive points, retry with a
 // fresh shuffle of the identity (same stream) on a loop or repeated edge.
@@ -149,6 +182,16 @@ bool make_topology(const gasloc_topology& topo, int n, uint64_t t, int32_t* row_
   }
   SplitMix64 rng(finalize64(topo.seed ^ finalize64(t)));
   Neighbours nb = self_only(n);
+  // App. B.1: the randomized selections may be restricted to the edges of an
+  // admissible graph (row-major n*n, symmetric); then weights are Metropolis.
+  const uint8_t* adm = topo.admissible;
+  if (adm && topo.kind != GASLOC_TOPO_ONE_PEER && topo.kind != GASLOC_TOPO_TWO_PEER) {
+    *err = "an admissible graph restricts only the ONE_PEER and TWO_PEER kinds";
+    return false;
+  }
+  auto allowed = [&](int a, int b) {
+    return adm == nullptr || adm[static_cast<size_t>(a) * static_cast<size_t>(n) + static_cast<size_t>(b)] != 0;
+  };
   switch (topo.kind) {
     case GASLOC_TOPO_RING:
       for (int i = 0; i < n; ++i) link(nb, i, (i + 1) % n);
@@ -174,14 +217,19 @@ bool make_topology(const gasloc_topology& topo, int n, uint64_t t, int32_t* row_
     case GASLOC_TOPO_ONE_PEER: {
       std::vector<int> s = identity(n);
       rng.permute(s);
-      for (int k = 0; k + 1 < n; k += 2) link(nb, s[static_cast<size_t>(k)], s[static_cast<size_t>(k) + 1]);
+      for (int k = 0; k + 1 < n; k += 2) {
+        const int a = s[static_cast<size_t>(k)], b = s[static_cast<size_t>(k) + 1];
+        if (allowed(a, b)) link(nb, a, b);
+      }
       break;
     }
     case GASLOC_TOPO_TWO_PEER: {
       std::vector<int> s = identity(n);
       rng.permute(s);
-      for (int k = 0; k < n; ++k)
-        link(nb, s[static_cast<size_t>(k)], s[static_cast<size_t>((k + 1) % n)]);
+      for (int k = 0; k < n; ++k) {
+        const int a = s[static_cast<size_t>(k)], b = s[static_cast<size_t>((k + 1) % n)];
+        if (allowed(a, b)) link(nb, a, b);
+      }
       break;
     }
     case GASLOC_TOPO_RANDOM_REGULAR: {
@@ -194,46 +242,71 @@ bool make_topology(const gasloc_topology& topo, int n, uint64_t t, int32_t* row_
         *err = "random regular graph: no simple graph after 100000 draws";
         return false;
       }
-      // Metropolis-Hastings weights: 1/(1 + max(d_i, d_j)) off the diagonal,
-      // the rest of the row on the diagonal.
-      int32_t k = 0;
-      row_ptr[0] = 0;
-      for (int i = 0; i < n; ++i) {
-        const auto& row = nb[static_cast<size_t>(i)];
-        const int di = static_cast<int>(row.size()) - 1;
-        double off_sum = 0.0;
-        for (int j : row) {
-          if (j == i) continue;
-          const int dj = static_cast<int>(nb[static_cast<size_t>(j)].size()) - 1;
-          off_sum += 1.0 / (1.0 + static_cast<double>(std::max(di, dj)));
-        }
-        for (int j : row) {
-          if (k >= cap) {
-            *err = "CSR capacity " + std::to_string(cap) + " too small";
-            return false;
-          }
-          double w;
-          if (j == i) {
-            w = 1.0 - off_sum;
-          } else {
-            const int dj = static_cast<int>(nb[static_cast<size_t>(j)].size()) - 1;
-            w = 1.0 / (1.0 + static_cast<double>(std::max(di, dj)));
-          }
-          col[k] = j;
-          val[k] = static_cast<float>(w);
-          ++k;
-        }
-        row_ptr[i + 1] = k;
-      }
-      *nnz = k;
-      return true;
+      return emit_metropolis(nb, row_ptr, col, val, cap, nnz, err);
     }
     default:
       *err = "topology kind " + std::to_string(topo.kind) + " has no generator";
       return false;
   }
   canonicalize(nb);
+  if (adm) return emit_metropolis(nb, row_ptr, col, val, cap, nnz, err);
   return emit_uniform(nb, row_ptr, col, val, cap, nnz, err);
+}
+
+// Section 3.2, "Fault tolerance": skipped exchanges.  An off-diagonal entry
+// (i, j) is removed when worker i or j is dead or the link between them
+// failed in either direction; worker i keeps that weight for itself.  The new
+// diagonal is the fp64 sum of the old diagonal and the removed weights (in
+// ascending column order), rounded once to fp32; a row gets a diagonal entry
+// if it had one or if that sum is nonzero.
+bool skip_exchanges(int n, const int32_t* rp, const int32_t* col, const float* val, const uint8_t* alive,
+                    const uint8_t* link_ok, int32_t* out_rp, int32_t* out_col, float* out_val, int32_t cap,
+                    int32_t* nnz, std::string* err) {
+  auto keep = [&](int i, int j) {
+    if (i == j) return true;
+    if (alive && (!alive[i] || !alive[j])) return false;
+    const size_t ij = static_cast<size_t>(i) * n + j, ji = static_cast<size_t>(j) * n + i;
+    return !(link_ok && (!link_ok[ij] || !link_ok[ji]));
+  };
+  std::vector<std::pair<int32_t, float>> row;
+  int32_t k_out = 0;
+  out_rp[0] = 0;
+  for (int i = 0; i < n; ++i) {
+    double diag = 0.0;
+    bool has_diag = false, moved = false;
+    float diag_val = 0.0f;
+    for (int32_t k = rp[i]; k < rp[i + 1]; ++k)
+      if (col[k] == i) {
+        diag += static_cast<double>(val[k]);
+        diag_val = val[k];
+        has_diag = true;
+      }
+    for (int32_t k = rp[i]; k < rp[i + 1]; ++k)
+      if (!keep(i, col[k])) {
+        diag += static_cast<double>(val[k]);
+        moved = true;
+      }
+    row.clear();
+    for (int32_t k = rp[i]; k < rp[i + 1]; ++k)
+      if (col[k] != i && keep(i, col[k])) row.emplace_back(col[k], val[k]);
+    if (has_diag || diag != 0.0) {
+      const float d = moved ? static_cast<float>(diag) : diag_val;
+      row.insert(std::lower_bound(row.begin(), row.end(), std::make_pair(static_cast<int32_t>(i), -1e30f)),
+                 std::make_pair(static_cast<int32_t>(i), d));
+    }
+    if (k_out + static_cast<int32_t>(row.size()) > cap) {
+      *err = "CSR capacity " + std::to_string(cap) + " too small";
+      return false;
+    }
+    for (const auto& e : row) {
+      out_col[k_out] = e.first;
+      out_val[k_out] = e.second;
+      ++k_out;
+    }
+    out_rp[i + 1] = k_out;
+  }
+  *nnz = k_out;
+  return true;
 }
 
 }  // namespace gasloc

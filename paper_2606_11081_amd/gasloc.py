@@ -35,7 +35,8 @@ class GaslocError(RuntimeError):
 
 
 class gasloc_topology(ctypes.Structure):
-    _fields_ = [("kind", ctypes.c_int32), ("degree", ctypes.c_int32), ("seed", ctypes.c_uint64)]
+    _fields_ = [("kind", ctypes.c_int32), ("degree", ctypes.c_int32), ("seed", ctypes.c_uint64),
+                ("admissible", ctypes.c_void_p)]
 
 
 class gasloc_hparams(ctypes.Structure):
@@ -74,6 +75,9 @@ _SIGNATURES = {
     "gasloc_make_topology": (ctypes.c_int, [ctypes.POINTER(gasloc_topology), _i32, _u64, _vp, _vp, _vp,
                                             _i32, ctypes.POINTER(_i32)]),
     "gasloc_validate_csr": (ctypes.c_int, [ctypes.POINTER(gasloc_csr), _i32]),
+    "gasloc_skip_exchanges": (ctypes.c_int, [ctypes.POINTER(gasloc_csr), _vp, _vp, _vp, _vp, _vp, _i32,
+                                             ctypes.POINTER(_i32)]),
+    "gasloc_set_alive": (ctypes.c_int, [_vp, _vp]),
     "gasloc_get_counters": (ctypes.c_int, [_vp, _vp, _vp, ctypes.POINTER(_i64)]),
     "gasloc_set_counters": (ctypes.c_int, [_vp, _vp, _vp, _i64]),
     "gasloc_lr_schedule": (ctypes.c_float, [ctypes.c_float, _i64, _i64, ctypes.c_float, ctypes.c_float,
@@ -121,8 +125,16 @@ def _host(a, dtype):
     return a, a.ctypes.data_as(ctypes.c_void_p)
 
 
-def make_topology_struct(kind="ring", seed=0, degree=3):
-    return gasloc_topology(TOPOLOGY[kind] if isinstance(kind, str) else int(kind), int(degree), int(seed))
+def make_topology_struct(kind="ring", seed=0, degree=3, admissible=None):
+    """Topology struct; with `admissible` (an [n, n] 0/1 array) the array is
+    kept alive on the struct as `_keep`."""
+    code = TOPOLOGY[kind] if isinstance(kind, str) else int(kind)
+    if admissible is None:
+        return gasloc_topology(code, int(degree), int(seed), None)
+    adm, ptr = _host(admissible, np.uint8)
+    t = gasloc_topology(code, int(degree), int(seed), ptr)
+    t._keep = adm
+    return t
 
 
 def make_hparams(beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1, outer_lr=0.7, outer_momentum=0.9,
@@ -231,6 +243,30 @@ def gasloc_validate_csr(W, n):
     del keep
 
 
+def gasloc_skip_exchanges(W, n, alive=None, link_ok=None):
+    csr, keep = make_csr(*W)
+    al = lk = None
+    if alive is not None:
+        al, alp = _host(alive, np.uint8)
+    if link_ok is not None:
+        lk, lkp = _host(link_ok, np.uint8)
+    rp, col, val = _csr_out(n, n * n)
+    nnz = _i32()
+    _check(library().gasloc_skip_exchanges(ctypes.byref(csr), None if al is None else alp,
+                                           None if lk is None else lkp, rp.ctypes.data, col.ctypes.data,
+                                           val.ctypes.data, n * n, ctypes.byref(nnz)))
+    del keep
+    return rp, col[:nnz.value].copy(), val[:nnz.value].copy()
+
+
+def gasloc_set_alive(ctx, alive=None):
+    keep = ptr = None
+    if alive is not None:
+        keep, ptr = _host(alive, np.uint8)
+    _check(library().gasloc_set_alive(ctx, ptr), ctx)
+    del keep
+
+
 def gasloc_get_counters(ctx, n):
     k = np.zeros(n, np.int64)
     stepped = np.zeros(n, np.uint8)
@@ -287,7 +323,7 @@ class GASLoC:
     """Owns one context plus its torch buffers; methods are the ABI calls."""
 
     def __init__(self, n, P, topology="ring", seed=0, degree=3, param_dtype="f32", device="cuda",
-                 stream=None, **hp):
+                 stream=None, admissible=None, **hp):
         import torch
 
         self.n, self.P, self.param_dtype = int(n), int(P), param_dtype
@@ -298,7 +334,7 @@ class GASLoC:
         self.ld = self.bufs["ld"]
         self.stream = torch.cuda.current_stream(device) if stream is None else stream
         b = self.bufs
-        self.ctx = gasloc_init(n, P, make_topology_struct(topology, seed, degree), hpar, b["x"], b["y"],
+        self.ctx = gasloc_init(n, P, make_topology_struct(topology, seed, degree, admissible), hpar, b["x"], b["y"],
                                b["m"], b["v"], b["u"], b["zp"], self.ld, self.stream.cuda_stream)
 
     def __getattr__(self, name):

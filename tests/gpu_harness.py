@@ -158,6 +158,10 @@ class Pair:
                     rb = np.asarray(ref)
                     rb = rb.view(np.uint32) if rb.dtype == np.float32 else rb
                     stats[name] = float(np.mean(gb == rb))
+        # the kernels take every rounding step in the fp32 oracle's order, so
+        # the fp32 state must be bit-identical, not merely within tolerance
+        if stats:
+            assert min(stats.values()) == 1.0, "%s: not bit-identical to the fp32 oracle: %s" % (tag, stats)
         if y_rows is not None and len(y_rows):
             rows = np.asarray(y_rows)
             gy = self.gather("y", rows=self.torch.as_tensor(rows, device="cuda"))

@@ -196,3 +196,60 @@ def test_lr_schedule_bit_exact_with_oracle(total, fracs):
         got = g.gasloc_lr_schedule(peak, step, total, w, s, f)
         exp = oracle.lr_schedule(peak, step, total, w, s, f)
         assert np.float32(got).view(np.uint32) == np.float32(exp).view(np.uint32), (step, got, exp)
+
+
+def _adjacency(n, p, seed):
+    rng = np.random.default_rng(seed)
+    A = np.triu((rng.random((n, n)) < p).astype(np.uint8), 1)
+    return (A + A.T).astype(np.uint8)
+
+
+@pytest.mark.parametrize("kind", ["one_peer", "two_peer"])
+@pytest.mark.parametrize("n,p", [(8, 0.5), (16, 0.3), (64, 0.1), (5, 1.0)])
+def test_restricted_schedule_bit_exact_with_oracle(kind, n, p):
+    A = _adjacency(n, p, n)
+    topo = g.make_topology_struct(kind, seed=3, admissible=A)
+    for t in range(60):
+        got = g.gasloc_make_topology(topo, n, t)
+        exp = oracle.topology_csr(kind, n, 3, t, admissible=A)
+        for a, b in zip(got, exp):
+            assert np.array_equal(a.view(np.uint32) if a.dtype == np.float32 else a,
+                                  b.view(np.uint32) if b.dtype == np.float32 else b)
+
+
+def test_admissible_only_for_random_peer_kinds():
+    with pytest.raises(g.GaslocError, match="admissible"):
+        g.gasloc_make_topology(g.make_topology_struct("ring", admissible=np.ones((4, 4))), 4, 0)
+    asym = np.zeros((4, 4), np.uint8)
+    asym[0, 1] = 1
+    with pytest.raises(g.GaslocError, match="symmetric"):
+        g.gasloc_init(4, 1024, g.make_topology_struct("one_peer", admissible=asym), g.make_hparams(), FAKE, FAKE,
+                      FAKE, FAKE, FAKE, FAKE, 1024)
+
+
+@pytest.mark.parametrize("kind", KINDS)
+def test_skip_exchanges_bit_exact_with_oracle(kind):
+    n = 12
+    rng = np.random.default_rng(11)
+    for t in range(20):
+        W = oracle.topology_csr(kind, n, 3, t, 3)
+        alive = (rng.random(n) > 0.25).astype(np.uint8)
+        link = (rng.random((n, n)) > 0.2).astype(np.uint8)
+        for al, lk in ((alive, None), (None, link), (alive, link), (None, None)):
+            got = g.gasloc_skip_exchanges(W, n, al, lk)
+            exp = oracle.skip_exchanges(W, n, al, lk)
+            assert np.array_equal(got[0], exp[0]) and np.array_equal(got[1], exp[1])
+            assert np.array_equal(got[2].view(np.uint32), exp[2].view(np.uint32))
+
+
+def test_skip_exchanges_on_a_csr_without_diagonal():
+    # a row without its own entry gets one only if weight is moved to it
+    rp = np.array([0, 2, 4, 6], np.int32)
+    col = np.array([1, 2, 0, 2, 0, 1], np.int32)
+    val = np.full(6, 0.5, np.float32)
+    alive = np.array([1, 1, 0], np.uint8)
+    got = g.gasloc_skip_exchanges((rp, col, val), 3, alive)
+    exp = oracle.skip_exchanges((rp, col, val), 3, alive)
+    for a, b in zip(got, exp):
+        assert np.array_equal(a, b)
+    assert list(got[0]) == [0, 2, 4, 5]

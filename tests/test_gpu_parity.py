@@ -205,6 +205,70 @@ def test_form_arguments_are_checked():
         d.local_step_gossip_round(grads, 0.01, 0)
 
 
+def test_dead_workers_match_the_oracle_with_skipped_exchanges():
+    import paper_2606_11081_amd as g
+
+    n, P = 16, 50_001
+    alive = np.ones(n, np.uint8)
+    alive[[2, 9]] = 0
+    # the library applies the mask itself; the oracle is given the masked W
+    # and the masked local steps explicitly
+    pair2 = Pair(n, P, "two_peer", "f32", gamma=0.1)
+    g.gasloc_set_alive(pair2.gpu.ctx, alive)
+    for t in range(3):
+        gi.fill_grads(pair2.grads, pair2.mu_i, pair2.step)
+        g_host = pair2.grads[:, pair2.cols_dev].cpu().numpy()
+        pair2.gpu.local_step(pair2.grads, pair2.lr)  # active = all, dead ones skipped
+        for o in pair2.oracles.values():
+            o.local_step(g_host, pair2.lr, alive)
+        pair2.step += 1
+        pair2.gpu.gossip_round(t)
+        for o in pair2.oracles.values():
+            o.gossip_round(t, csr=oracle.skip_exchanges(o.csr(t), n, alive, precision=o.precision))
+        reduction_close(pair2.gpu.consensus_error(), pair2.oracles["f32"].consensus_error(), "CE round %d" % t)
+    k, _, _ = pair2.gpu.counters()
+    assert list(k[[2, 9]]) == [0, 0] and all(k[alive == 1] == 3)
+    pair2.check_state(tag="dead workers")
+
+
+def test_nan_gradient_spreads_only_along_the_round_edges():
+    import torch
+
+    n, P = 8, 4_096
+    pair = Pair(n, P, "one_peer", "f32", gamma=0.0, precisions=("f32",))
+    gi.fill_grads(pair.grads, pair.mu_i, 0)
+    bad = 5
+    pair.grads[bad, 100] = float("nan")
+    pair.gpu.local_step(pair.grads, pair.lr)
+    pair.gpu.gossip_round(0)
+    torch.cuda.synchronize()
+    x = pair.gpu.x[:, :P].cpu().numpy()
+    W = oracle.csr_to_dense(*oracle.topology_csr("one_peer", n, gi.SEED_TOPOLOGY, 0), n)
+    poisoned = np.isnan(x[:, 100])
+    assert np.array_equal(poisoned, W[:, bad] != 0), "NaN reaches exactly the workers that read worker %d" % bad
+    assert not np.isnan(np.delete(x, 100, axis=1)).any(), "other columns stay finite"
+    assert np.isnan(pair.gpu.consensus_error())
+
+
+def test_restricted_schedule_on_device():
+    import paper_2606_11081_amd as g
+
+    n, P = 16, 10_007
+    rng = np.random.default_rng(5)
+    A = np.triu((rng.random((n, n)) < 0.3).astype(np.uint8), 1)
+    A = A + A.T
+    pair = Pair(n, P, "two_peer", "f32", gamma=0.1)
+    gpu2 = g.GASLoC(n, P, topology="two_peer", seed=gi.SEED_TOPOLOGY, admissible=A)
+    for t in range(4):
+        got = g.gasloc_topology_csr(gpu2.ctx, t, n)
+        exp = oracle.topology_csr("two_peer", n, gi.SEED_TOPOLOGY, t, admissible=A)
+        for a, b in zip(got, exp):
+            assert np.array_equal(a, b)
+        pair.local_step()
+        pair.gossip_round(t, W=exp)
+    pair.check_state(tag="restricted")
+
+
 def test_explicit_nonsymmetric_csr_and_identity():
     n, P = 6, 5003
     rng = np.random.default_rng(3)
