@@ -14,7 +14,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libgasloc.so")
-SOURCES = ["kernels.hip", "runtime.cpp", "topology.cpp", "schedule.cpp"]
+SOURCES = ["kernels.hip", "runtime.cpp", "topology.cpp", "schedule.cpp", "plan.cpp"]
 ARCH = "gfx950"
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-ffp-contract=off",

@@ -6,6 +6,7 @@
 
 #include <cstdint>
 #include <string>
+#include <vector>
 
 #include "gasloc.h"
 
@@ -15,6 +16,12 @@ constexpr int kMaxReplicas = 64;
 
 bool make_topology(const gasloc_topology& topo, int n, uint64_t t, int32_t* row_ptr, int32_t* col,
                    float* val, int32_t cap, int32_t* nnz, std::string* err);
+// Visit plan of a round for the slot-reusing kernel (plan.cpp); the plan is
+// checked by verify_plan before it is returned.
+bool plan_round(int n, const int32_t* rp, const int32_t* col, const float* val, std::vector<int32_t>* ops,
+                int* slots_used, std::string* err);
+bool verify_plan(int n, const int32_t* rp, const int32_t* col, const float* val, const int32_t* ops, int len,
+                 int slots, std::string* err);
 bool skip_exchanges(int n, const int32_t* rp, const int32_t* col, const float* val, const uint8_t* alive,
                     const uint8_t* link_ok, int32_t* out_rp, int32_t* out_col, float* out_val, int32_t cap,
                     int32_t* nnz, std::string* err);
@@ -61,6 +68,11 @@ struct GossipArgs {
   int32_t store_zp;     // keep z for the next round's gamma term
   uint64_t stepped;     // bit i: worker i took local steps since the last round
 
+  // planned visit order (k_gossip_planned only): see plan.cpp
+  const int32_t* ops;
+  int32_t ops_len;
+  int32_t slots;
+
   // Fused last local step (the fused kernel only): every worker i with bit i
   // of `active` first takes one AdamW step from its live iterate; the new
   // iterate feeds delta directly and is never written back (it is logically
@@ -86,6 +98,9 @@ struct LaunchShape {
 hipError_t launch_local_adamw(const AdamArgs& a, int dtype, int blocks_per_worker, hipStream_t stream);
 hipError_t launch_gossip_round(const GossipArgs& a, int dtype, bool fused, int form,
                                const LaunchShape& shape, hipStream_t stream);
+hipError_t launch_gossip_planned(const GossipArgs& a, int dtype, bool fused, const LaunchShape& shape,
+                                 hipStream_t stream);
+size_t planned_lds_bytes(int slots, int ops_len, const LaunchShape& shape);
 hipError_t launch_consensus_error(const void* x, int dtype, int64_t ld, int n, int64_t p_begin,
                                   int64_t p_end, double* partials, int blocks, hipStream_t stream);
 hipError_t launch_finalize(const double* partials, int count, double* out, hipStream_t stream);

@@ -491,6 +491,144 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// The EQ round with a host-planned visit order (plan.cpp): each step computes
+// the z of the workers first read by its row into free LDS slots, then emits
+// the row.  LDS holds `slots` values per column instead of n, so sparse
+// graphs keep many more columns in flight per CU.  Per element the
+// arithmetic is exactly that of k_gossip_round<..., GASLOC_FORM_EQ>.
+// ---------------------------------------------------------------------------
+
+template <int DT, int V, int R, bool FUSED>
+__global__ __launch_bounds__(256) void k_gossip_planned(GossipArgs a) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int nt = blockDim.x;
+  const int tid = threadIdx.x;
+  float* zs = reinterpret_cast<float*>(lds);  // [slots][nt][V]
+  int32_t* ops = reinterpret_cast<int32_t*>(lds + static_cast<size_t>(a.slots) * nt * V * sizeof(float));
+  for (int k = tid; k < a.ops_len; k += nt) ops[k] = a.ops[k];
+  __syncthreads();
+
+  const double inv_n = 1.0 / static_cast<double>(a.n);
+  const int steps = ops[0];
+  const int64_t groups = (a.P + V - 1) / V;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * nt;
+  double ce = 0.0;
+  for (int64_t gi = static_cast<int64_t>(blockIdx.x) * nt + tid; gi < groups; gi += stride) {
+    const int64_t p = gi * V;
+    const int cnt = static_cast<int>(a.P - p < V ? a.P - p : V);
+    auto slot = [&](int s) { return zs + (static_cast<size_t>(s) * nt + tid) * V; };
+    double shift[V], s[V], q[V];
+    int pc = 1;
+    for (int st = 0; st < steps; ++st) {
+      const int row = ops[pc];
+      const int npre = ops[pc + 1];
+      const int pre = pc + 2;
+      const int ent = pre + 2 * npre;
+      const int nent = ops[ent];
+      const int own = ops[ent + 1 + 2 * nent];
+      pc = ent + 2 + 2 * nent;
+      const int64_t er = static_cast<int64_t>(row) * a.ld + p;
+      float zpv[V];
+      if (a.apply_gamma) load_f32<V>(a.zp + er, cnt, zpv);
+
+      // post-outer iterates of the workers this row reads first
+      for (int q0 = 0; q0 < npre; q0 += R) {
+        constexpr int RF = FUSED ? R : 1;
+        float xv[R][V], yv[R][V], uv[R][V];
+        float gv[RF][V], mv[RF][V], vv[RF][V];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          if (q0 + r >= npre) break;
+          const int j = ops[pre + 2 * (q0 + r)];
+          const int64_t e = static_cast<int64_t>(j) * a.ld + p;
+          load_params<DT, V>(a.x, e, cnt, xv[r]);
+          if ((a.stepped >> j) & 1ull) {
+            load_params<DT, V>(a.y, e, cnt, yv[r]);
+          } else {
+#pragma unroll
+            for (int c = 0; c < V; ++c) yv[r][c] = xv[r][c];
+          }
+          if constexpr (FUSED) {
+            if ((a.active >> j) & 1ull) {
+              load_f32<V>(a.g + static_cast<int64_t>(j) * a.gld + p, cnt, gv[r]);
+              load_f32<V>(a.m + e, cnt, mv[r]);
+              load_f32<V>(a.v + e, cnt, vv[r]);
+            }
+          }
+          if (a.use_u) {
+            load_f32<V>(a.u + e, cnt, uv[r]);
+          } else {
+#pragma unroll
+            for (int c = 0; c < V; ++c) uv[r][c] = 0.0f;
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          if (q0 + r >= npre) break;
+          const int j = ops[pre + 2 * (q0 + r)];
+          const int64_t e = static_cast<int64_t>(j) * a.ld + p;
+          if constexpr (FUSED) {
+            if ((a.active >> j) & 1ull) {
+              const float s1 = a.s1[j], c2 = a.c2[j];
+#pragma unroll
+              for (int c = 0; c < V; ++c)
+                yv[r][c] = as_stored<DT>(adamw_element(yv[r][c], gv[r][c], mv[r][c], vv[r][c], a.c_wd, a.b1,
+                                                       a.omb1, a.b2, a.omb2, a.eps, s1, c2));
+              store_f32<V>(a.m + e, cnt, mv[r]);
+              store_f32<V>(a.v + e, cnt, vv[r]);
+            }
+          }
+          float* out = slot(ops[pre + 2 * (q0 + r) + 1]);
+#pragma unroll
+          for (int c = 0; c < V; ++c)
+            out[c] = outer_step(xv[r][c], xv[r][c] - yv[r][c], uv[r][c], a.mu, a.eta, a.nesterov);
+          if (a.use_u) store_f32<V>(a.u + e, cnt, uv[r]);
+        }
+      }
+
+      // the row: sum_k W_rk z_k in CSR order (+ gamma (z_r - zp_r)), zp_r = z_r
+      float acc[V];
+#pragma unroll
+      for (int c = 0; c < V; ++c) acc[c] = 0.0f;
+      for (int k = 0; k < nent; ++k) {
+        const float* zk = slot(ops[ent + 1 + 2 * k]);
+        const float w = __int_as_float(ops[ent + 2 + 2 * k]);
+#pragma unroll
+        for (int c = 0; c < V; ++c) acc[c] = acc[c] + w * zk[c];
+      }
+      const float* zo = slot(own);
+      float zcur[V];
+#pragma unroll
+      for (int c = 0; c < V; ++c) zcur[c] = zo[c];
+      if (a.apply_gamma) {
+#pragma unroll
+        for (int c = 0; c < V; ++c) acc[c] = acc[c] + a.gamma * (zcur[c] - zpv[c]);
+      }
+      if (a.store_zp) store_f32<V>(a.zp + er, cnt, zcur);
+      float kept[V];
+      store_params<DT, V>(a.x, er, cnt, acc, kept);
+#pragma unroll
+      for (int c = 0; c < V; ++c) {
+        const double xd = static_cast<double>(kept[c]);
+        if (st == 0) {
+          shift[c] = xd;
+          s[c] = 0.0;
+          q[c] = 0.0;
+        }
+        const double dv = xd - shift[c];
+        s[c] += dv;
+        q[c] += dv * dv;
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < V; ++c)
+      if (c < cnt) ce += q[c] - s[c] * s[c] * inv_n;
+  }
+  const double total = block_sum(ce);
+  if (tid == 0) a.partials[blockIdx.x] = total;
+}
+
+// ---------------------------------------------------------------------------
 // a5 standalone: consensus error of the stored x over columns [p_begin, p_end)
 // ---------------------------------------------------------------------------
 
@@ -609,6 +747,36 @@ hipError_t launch_local_adamw(const AdamArgs& a, int dtype, int blocks_per_worke
   else
     hipLaunchKernelGGL((k_local_adamw<GASLOC_F32>), grid, dim3(256), 0, stream, a);
   return hipGetLastError();
+}
+
+size_t planned_lds_bytes(int slots, int ops_len, const LaunchShape& s) {
+  return static_cast<size_t>(slots) * s.threads * s.vec * sizeof(float) + static_cast<size_t>(ops_len) * 4;
+}
+
+template <int DT, int V, bool FUSED>
+hipError_t launch_planned_typed(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
+  const size_t lds = planned_lds_bytes(a.slots, a.ops_len, s);
+  if (s.batch <= 2)
+    hipLaunchKernelGGL((k_gossip_planned<DT, V, 2, FUSED>), dim3(s.blocks), dim3(s.threads), lds, stream, a);
+  else
+    hipLaunchKernelGGL((k_gossip_planned<DT, V, 4, FUSED>), dim3(s.blocks), dim3(s.threads), lds, stream, a);
+  return hipGetLastError();
+}
+
+template <int DT, bool FUSED>
+hipError_t launch_planned_vec(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
+  if (s.vec == 4) return launch_planned_typed<DT, 4, FUSED>(a, s, stream);
+  if (s.vec == 2) return launch_planned_typed<DT, 2, FUSED>(a, s, stream);
+  return launch_planned_typed<DT, 1, FUSED>(a, s, stream);
+}
+
+hipError_t launch_gossip_planned(const GossipArgs& a, int dtype, bool fused, const LaunchShape& s,
+                                 hipStream_t stream) {
+  if (dtype == GASLOC_BF16)
+    return fused ? launch_planned_vec<GASLOC_BF16, true>(a, s, stream)
+                 : launch_planned_vec<GASLOC_BF16, false>(a, s, stream);
+  return fused ? launch_planned_vec<GASLOC_F32, true>(a, s, stream)
+               : launch_planned_vec<GASLOC_F32, false>(a, s, stream);
 }
 
 hipError_t launch_gossip_round(const GossipArgs& a, int dtype, bool fused, int form, const LaunchShape& s,

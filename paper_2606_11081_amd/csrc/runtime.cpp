@@ -43,6 +43,11 @@ size_t csr_stage_bytes(int n) {
   return sizeof(int32_t) * static_cast<size_t>(n + 1) + (sizeof(int32_t) + sizeof(float)) * n * n;
 }
 
+// Largest visit plan (plan.cpp) for n workers: 1 + 6n + 2 nnz int32 values.
+size_t plan_stage_bytes(int n) { return sizeof(int32_t) * (1 + 6 * static_cast<size_t>(n) + 2 * n * n); }
+
+size_t stage_bytes(int n) { return std::max(csr_stage_bytes(n), plan_stage_bytes(n)); }
+
 }  // namespace
 
 struct gasloc_ctx {
@@ -60,6 +65,7 @@ struct gasloc_ctx {
   bool any_dead = false;
   std::vector<int32_t> skip_rp, skip_col;  // scratch for skipped exchanges
   std::vector<float> skip_val;
+  std::vector<int32_t> plan_ops;  // visit plan of the current round
   std::vector<int64_t> k;         // AdamW step count per worker
   std::vector<uint8_t> stepped;   // local steps taken since the last round
   int64_t rounds_done = 0;
@@ -242,6 +248,33 @@ gasloc_status upload_csr(gasloc_ctx* c, const int32_t* row_ptr, const int32_t* c
   return GASLOC_OK;
 }
 
+// Copies a visit plan into the next pinned slot and enqueues its upload.
+gasloc_status upload_plan(gasloc_ctx* c, const std::vector<int32_t>& ops) {
+  const int slot = c->stage_next;
+  c->stage_next = (c->stage_next + 1) % kStageSlots;
+  if (c->stage_used[slot]) HIP_TRY(c, hipEventSynchronize(c->stage_done[slot]));
+  const size_t bytes = sizeof(int32_t) * ops.size();
+  std::memcpy(c->h_stage[slot], ops.data(), bytes);
+  HIP_TRY(c, hipMemcpyAsync(c->d_csr, c->h_stage[slot], bytes, hipMemcpyHostToDevice, c->stream));
+  HIP_TRY(c, hipEventRecord(c->stage_done[slot], c->stream));
+  c->stage_used[slot] = true;
+  return GASLOC_OK;
+}
+
+// Which EQ-form kernel runs a round: the phase kernel keeps every worker's z
+// in LDS; the planned kernel (plan.cpp) keeps only the live ones.  Measured
+// on MI355X: planned is 2.3x faster at n=64 (1-Peer), 1.4x at n=32 (3-regular),
+// 1% faster at n=16 and even at n=8; when the plan needs a slot per worker
+// (dense W) the two hold the same data and the phase kernel is kept.
+// Override for tuning sweeps: GASLOC_GOSSIP_KERNEL=phase|planned.
+bool use_planned(const gasloc_ctx& c, int slots) {
+  if (const char* env = std::getenv("GASLOC_GOSSIP_KERNEL")) {
+    if (std::strcmp(env, "phase") == 0) return false;
+    if (std::strcmp(env, "planned") == 0) return true;
+  }
+  return slots < c.n;
+}
+
 gasloc_status reduce_cols(gasloc_ctx* c, int64_t p0, int64_t p1) {
   HIP_TRY(c, gasloc::launch_consensus_error(c->buf.x, c->hp.param_dtype, c->buf.ld, c->n, p0, p1,
                                             c->d_partials, c->reduce_blocks, c->stream));
@@ -337,15 +370,38 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
     val = c->skip_val.data();
   }
   DeviceGuard guard(c->device);
-  gasloc::LaunchShape shape = pick_gossip_shape(*c, nnz);
-  if (step) shape.batch = 4;
-  shape.blocks = gossip_blocks(*c, shape, nnz);
-  apply_shape_override(&shape);
-  if (shape.blocks == 0) shape.blocks = gossip_blocks(*c, shape, nnz);
+  bool planned = false;
+  int slots = 0;
+  if (c->hp.round_form == GASLOC_FORM_EQ) {
+    std::string err;
+    if (!gasloc::plan_round(c->n, rp, col, val, &c->plan_ops, &slots, &err)) return fail(c, GASLOC_EINVAL, err);
+    planned = use_planned(*c, slots);
+  }
+  gasloc::LaunchShape shape;
+  size_t lds = 0;
+  if (planned) {
+    const int ops_len = static_cast<int>(c->plan_ops.size());
+    shape = gasloc::LaunchShape{4, 256, 0, 4};
+    while (shape.threads > 64 && gasloc::planned_lds_bytes(slots, ops_len, shape) + gasloc::kStaticLds >
+                                     std::min(c->lds_per_cu / 2, c->lds_per_block_max))
+      shape.threads /= 2;
+    apply_shape_override(&shape);
+    lds = gasloc::planned_lds_bytes(slots, ops_len, shape) + gasloc::kStaticLds;
+    const int per_cu = std::max(1, static_cast<int>(std::min<size_t>(c->lds_per_cu / lds, 8)));
+    const int64_t needed = ((c->P + shape.vec - 1) / shape.vec + shape.threads - 1) / shape.threads;
+    if (shape.blocks == 0)
+      shape.blocks = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(needed, int64_t(c->cus) * per_cu)));
+  } else {
+    shape = pick_gossip_shape(*c, nnz);
+    if (step) shape.batch = 4;
+    shape.blocks = gossip_blocks(*c, shape, nnz);
+    apply_shape_override(&shape);
+    if (shape.blocks == 0) shape.blocks = gossip_blocks(*c, shape, nnz);
+    lds = gasloc::gossip_lds_bytes(c->n, nnz, shape) + gasloc::kStaticLds;
+  }
   shape.blocks = std::min(shape.blocks, c->partial_cap);
-  if (gasloc::gossip_lds_bytes(c->n, nnz, shape) + gasloc::kStaticLds > c->lds_per_block_max)
-    return fail(c, GASLOC_EINVAL, "gossip shape exceeds the device's LDS per workgroup");
-  gasloc_status st = upload_csr(c, rp, col, val, nnz);
+  if (lds > c->lds_per_block_max) return fail(c, GASLOC_EINVAL, "gossip shape exceeds the device's LDS per workgroup");
+  gasloc_status st = planned ? upload_plan(c, c->plan_ops) : upload_csr(c, rp, col, val, nnz);
   if (st != GASLOC_OK) return st;
 
   gasloc::GossipArgs a{};
@@ -386,8 +442,15 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
     std::memcpy(a.c2, step->c2, sizeof a.c2);
   }
   a.partials = c->d_partials;
-  HIP_TRY(c, gasloc::launch_gossip_round(a, c->hp.param_dtype, step != nullptr, c->hp.round_form, shape,
-                                         c->stream));
+  if (planned) {
+    a.ops = reinterpret_cast<const int32_t*>(c->d_csr);
+    a.ops_len = static_cast<int32_t>(c->plan_ops.size());
+    a.slots = slots;
+    HIP_TRY(c, gasloc::launch_gossip_planned(a, c->hp.param_dtype, step != nullptr, shape, c->stream));
+  } else {
+    HIP_TRY(c, gasloc::launch_gossip_round(a, c->hp.param_dtype, step != nullptr, c->hp.round_form, shape,
+                                           c->stream));
+  }
   HIP_TRY(c, gasloc::launch_finalize(c->d_partials, shape.blocks, c->d_ce, c->stream));
   if (step) {
     for (int i = 0; i < c->n; ++i)
@@ -495,14 +558,14 @@ gasloc_status gasloc_init(int32_t n, int64_t P, const gasloc_topology* topology,
   c->reduce_blocks = std::min(kMaxGridBlocks, c->cus * 4);
   c->partial_cap = kMaxGridBlocks;
 
-  if ((e = hipMalloc(&c->d_csr, csr_stage_bytes(n))) != hipSuccess) return init_fail(e, "hipMalloc csr");
+  if ((e = hipMalloc(&c->d_csr, stage_bytes(n))) != hipSuccess) return init_fail(e, "hipMalloc csr");
   if ((e = hipMalloc(&c->d_partials, sizeof(double) * c->partial_cap)) != hipSuccess)
     return init_fail(e, "hipMalloc partials");
   if ((e = hipMalloc(&c->d_ce, sizeof(double))) != hipSuccess) return init_fail(e, "hipMalloc ce");
   if ((e = hipHostMalloc(&c->h_ce, sizeof(double), hipHostMallocDefault)) != hipSuccess)
     return init_fail(e, "hipHostMalloc ce");
   for (int i = 0; i < kStageSlots; ++i) {
-    if ((e = hipHostMalloc(&c->h_stage[i], csr_stage_bytes(n), hipHostMallocDefault)) != hipSuccess)
+    if ((e = hipHostMalloc(&c->h_stage[i], stage_bytes(n), hipHostMallocDefault)) != hipSuccess)
       return init_fail(e, "hipHostMalloc staging");
     if ((e = hipEventCreateWithFlags(&c->stage_done[i], hipEventDisableTiming)) != hipSuccess)
       return init_fail(e, "hipEventCreate");
