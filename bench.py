@@ -23,8 +23,9 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, AMD specification
 METRIC = "replica-param updates/s per gossip round; achieved HBM GB/s vs peak"
 DEFAULT_WORKLOAD = "onepeer-exp-n16-p350m"
-# the kernels and the code that picks their launch shapes
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_11081_amd", "csrc", f) for f in ("kernels.hip", "runtime.cpp")]
+# the kernels and the code that picks them and their launch shapes
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_11081_amd", "csrc", f)
+                  for f in ("kernels.hip", "runtime.cpp", "plan.cpp")]
 
 
 def log(msg):
@@ -72,7 +73,7 @@ def fused_bytes_per_rp(sp, gamma, active, stepped, with_u=True):
 def read_traffic(kernel, workload):
     """HBM bytes per dispatch from a committed rocprofv3 --pmc summary, or None
     if absent or taken on a different kernel source."""
-    path = os.path.join(ROOT, "profiles", "%s_%s_pmc.md" % (kernel, workload))
+    path = os.path.join(ROOT, "profiles", "%s_%s_pmc.md" % (kernel, workload))  # kernel: a kernel or role name
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -240,7 +241,7 @@ def main():
         dom, dom_bytes = "k_local_adamw", float(np.mean([r * adam_bytes for r in adam_rp]))
         dom_ms = float(np.mean(adam_ms))
     else:
-        dom = "k_gossip_round" if not args.fuse else "k_gossip_round_fused"
+        dom = "fused_round" if args.fuse else "gossip_round"
         dom_bytes, dom_ms = round_bytes, float(np.mean(round_ms))
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
@@ -260,11 +261,12 @@ def main():
                    "gamma": w.gamma, "param_dtype": w.param_dtype, "state_dtype": "f32",
                    "last_local_step_fused": bool(args.fuse)},
         "roofline": roofline,
-        "gossip_round": {"kernel": "k_gossip_round", "rp_updates_per_s": w.n * w.P / (gossip_ms * 1e-3),
+        "gossip_round": {"role": "gossip round alone (library-chosen gossip kernel + CSR/plan upload + finalize)",
+                         "rp_updates_per_s": w.n * w.P / (gossip_ms * 1e-3),
                          "ms": round(gossip_ms, 4), "GBps": round(gossip_gbps, 1),
                          "frac_of_peak": round(gossip_gbps / PEAK_HBM_GBPS, 4), "bytes_per_rp": gossip_bytes,
-                         "traffic": read_traffic("k_gossip_round", w.name)},
-        "round_kernel": {"kernel": "k_gossip_round_fused" if args.fuse else "k_gossip_round",
+                         "traffic": read_traffic("gossip_round", w.name)},
+        "round_kernel": {"role": "fused_round" if args.fuse else "gossip_round",
                          "ms": round(float(np.mean(round_ms)), 4), "GBps": round(round_gbps, 1),
                          "frac_of_peak": round(round_gbps / PEAK_HBM_GBPS, 4),
                          "bytes_per_launch": int(round_bytes)},

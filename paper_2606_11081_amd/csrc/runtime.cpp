@@ -263,16 +263,17 @@ gasloc_status upload_plan(gasloc_ctx* c, const std::vector<int32_t>& ops) {
 
 // Which EQ-form kernel runs a round: the phase kernel keeps every worker's z
 // in LDS; the planned kernel (plan.cpp) keeps only the live ones.  Measured
-// on MI355X: planned is 2.3x faster at n=64 (1-Peer), 1.4x at n=32 (3-regular),
-// 1% faster at n=16 and even at n=8; when the plan needs a slot per worker
-// (dense W) the two hold the same data and the phase kernel is kept.
+// on MI355X: planned is 2.3x faster at n=64 (1-Peer) and 1.4x at n=32
+// (3-regular), where LDS limits the phase kernel; at n <= 16 the phase
+// kernel fits and keeps more loads in flight (fused round at n=16: 45.0 vs
+// 48.2 ms), and a dense W needs a slot per worker anyway.
 // Override for tuning sweeps: GASLOC_GOSSIP_KERNEL=phase|planned.
 bool use_planned(const gasloc_ctx& c, int slots) {
   if (const char* env = std::getenv("GASLOC_GOSSIP_KERNEL")) {
     if (std::strcmp(env, "phase") == 0) return false;
     if (std::strcmp(env, "planned") == 0) return true;
   }
-  return slots < c.n;
+  return c.n > 16 && slots < c.n;
 }
 
 gasloc_status reduce_cols(gasloc_ctx* c, int64_t p0, int64_t p1) {
