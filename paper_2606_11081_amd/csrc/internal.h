@@ -16,12 +16,14 @@ constexpr int kMaxReplicas = 64;
 
 bool make_topology(const gasloc_topology& topo, int n, uint64_t t, int32_t* row_ptr, int32_t* col,
                    float* val, int32_t cap, int32_t* nnz, std::string* err);
-// Visit plan of a round for the slot-reusing kernel (plan.cpp); the plan is
-// checked by verify_plan before it is returned.
-bool plan_round(int n, const int32_t* rp, const int32_t* col, const float* val, std::vector<int32_t>* ops,
-                int* slots_used, std::string* err);
+// Visit plan of a round for the slot-reusing kernel (plan.cpp): super-steps
+// of at most max_pre new z values and at most max_rows (<= kPlanRows) rows;
+// the plan is checked by verify_plan before it is returned.
+constexpr int kPlanRows = 4;
+bool plan_round(int n, const int32_t* rp, const int32_t* col, const float* val, int max_pre, int max_rows,
+                std::vector<int32_t>* ops, int* slots_used, std::string* err);
 bool verify_plan(int n, const int32_t* rp, const int32_t* col, const float* val, const int32_t* ops, int len,
-                 int slots, std::string* err);
+                 int slots, int max_rows, std::string* err);
 bool skip_exchanges(int n, const int32_t* rp, const int32_t* col, const float* val, const uint8_t* alive,
                     const uint8_t* link_ok, int32_t* out_rp, int32_t* out_col, float* out_val, int32_t cap,
                     int32_t* nnz, std::string* err);

@@ -491,9 +491,10 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// The EQ round with a host-planned visit order (plan.cpp): each step computes
-// the z of the workers first read by its row into free LDS slots, then emits
-// the row.  LDS holds `slots` values per column instead of n, so sparse
+// The EQ round with a host-planned visit order (plan.cpp): each super-step
+// computes the z of the workers first read by its rows into free LDS slots
+// (loads of up to R workers and the rows' zp in flight together), then emits
+// up to kPlanRows rows.  LDS holds `slots` values per column instead of n, so sparse
 // graphs keep many more columns in flight per CU.  Per element the
 // arithmetic is exactly that of k_gossip_round<..., GASLOC_FORM_EQ>.
 // ---------------------------------------------------------------------------
@@ -518,20 +519,26 @@ __global__ __launch_bounds__(256) void k_gossip_planned(GossipArgs a) {
     const int cnt = static_cast<int>(a.P - p < V ? a.P - p : V);
     auto slot = [&](int s) { return zs + (static_cast<size_t>(s) * nt + tid) * V; };
     double shift[V], s[V], q[V];
+    bool first_row = true;
     int pc = 1;
     for (int st = 0; st < steps; ++st) {
-      const int row = ops[pc];
-      const int npre = ops[pc + 1];
-      const int pre = pc + 2;
-      const int ent = pre + 2 * npre;
-      const int nent = ops[ent];
-      const int own = ops[ent + 1 + 2 * nent];
-      pc = ent + 2 + 2 * nent;
-      const int64_t er = static_cast<int64_t>(row) * a.ld + p;
-      float zpv[V];
-      if (a.apply_gamma) load_f32<V>(a.zp + er, cnt, zpv);
+      const int npre = ops[pc];
+      const int pre = pc + 1;
+      int rq = pre + 2 * npre;
+      const int nrows = ops[rq++];
+      // the consensus-momentum reads of this super-step's rows go out first
+      int rowpos[kPlanRows];
+      float zpv[kPlanRows][V];
+#pragma unroll
+      for (int rr = 0; rr < kPlanRows; ++rr) {
+        if (rr >= nrows) break;
+        rowpos[rr] = rq;
+        if (a.apply_gamma) load_f32<V>(a.zp + static_cast<int64_t>(ops[rq]) * a.ld + p, cnt, zpv[rr]);
+        rq += 3 + 2 * ops[rq + 1];
+      }
+      pc = rq;
 
-      // post-outer iterates of the workers this row reads first
+      // post-outer iterates of the workers first read in this super-step
       for (int q0 = 0; q0 < npre; q0 += R) {
         constexpr int RF = FUSED ? R : 1;
         float xv[R][V], yv[R][V], uv[R][V];
@@ -586,38 +593,47 @@ __global__ __launch_bounds__(256) void k_gossip_planned(GossipArgs a) {
         }
       }
 
-      // the row: sum_k W_rk z_k in CSR order (+ gamma (z_r - zp_r)), zp_r = z_r
-      float acc[V];
+      // the rows: sum_k W_rk z_k in CSR order (+ gamma (z_r - zp_r)), zp_r = z_r
 #pragma unroll
-      for (int c = 0; c < V; ++c) acc[c] = 0.0f;
-      for (int k = 0; k < nent; ++k) {
-        const float* zk = slot(ops[ent + 1 + 2 * k]);
-        const float w = __int_as_float(ops[ent + 2 + 2 * k]);
+      for (int rr = 0; rr < kPlanRows; ++rr) {
+        if (rr >= nrows) break;
+        const int at = rowpos[rr];
+        const int row = ops[at];
+        const int nent = ops[at + 1];
+        const int64_t er = static_cast<int64_t>(row) * a.ld + p;
+        float acc[V];
 #pragma unroll
-        for (int c = 0; c < V; ++c) acc[c] = acc[c] + w * zk[c];
-      }
-      const float* zo = slot(own);
-      float zcur[V];
+        for (int c = 0; c < V; ++c) acc[c] = 0.0f;
+        for (int kk = 0; kk < nent; ++kk) {
+          const float* zk = slot(ops[at + 2 + 2 * kk]);
+          const float w = __int_as_float(ops[at + 3 + 2 * kk]);
 #pragma unroll
-      for (int c = 0; c < V; ++c) zcur[c] = zo[c];
-      if (a.apply_gamma) {
-#pragma unroll
-        for (int c = 0; c < V; ++c) acc[c] = acc[c] + a.gamma * (zcur[c] - zpv[c]);
-      }
-      if (a.store_zp) store_f32<V>(a.zp + er, cnt, zcur);
-      float kept[V];
-      store_params<DT, V>(a.x, er, cnt, acc, kept);
-#pragma unroll
-      for (int c = 0; c < V; ++c) {
-        const double xd = static_cast<double>(kept[c]);
-        if (st == 0) {
-          shift[c] = xd;
-          s[c] = 0.0;
-          q[c] = 0.0;
+          for (int c = 0; c < V; ++c) acc[c] = acc[c] + w * zk[c];
         }
-        const double dv = xd - shift[c];
-        s[c] += dv;
-        q[c] += dv * dv;
+        const float* zo = slot(ops[at + 2 + 2 * nent]);
+        float zcur[V];
+#pragma unroll
+        for (int c = 0; c < V; ++c) zcur[c] = zo[c];
+        if (a.apply_gamma) {
+#pragma unroll
+          for (int c = 0; c < V; ++c) acc[c] = acc[c] + a.gamma * (zcur[c] - zpv[rr][c]);
+        }
+        if (a.store_zp) store_f32<V>(a.zp + er, cnt, zcur);
+        float kept[V];
+        store_params<DT, V>(a.x, er, cnt, acc, kept);
+#pragma unroll
+        for (int c = 0; c < V; ++c) {
+          const double xd = static_cast<double>(kept[c]);
+          if (first_row) {
+            shift[c] = xd;
+            s[c] = 0.0;
+            q[c] = 0.0;
+          }
+          const double dv = xd - shift[c];
+          s[c] += dv;
+          q[c] += dv * dv;
+        }
+        first_row = false;
       }
     }
 #pragma unroll

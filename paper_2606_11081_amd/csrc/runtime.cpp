@@ -21,6 +21,7 @@ using gasloc::kMaxReplicas;
 namespace {
 
 constexpr int kStageSlots = 4;      // pinned CSR staging slots, reused round-robin
+constexpr int kPlanBatch = 4;       // new z values per super-step of a round plan
 constexpr int kMaxGridBlocks = 16384;
 
 thread_local std::string g_thread_error;
@@ -43,8 +44,10 @@ size_t csr_stage_bytes(int n) {
   return sizeof(int32_t) * static_cast<size_t>(n + 1) + (sizeof(int32_t) + sizeof(float)) * n * n;
 }
 
-// Largest visit plan (plan.cpp) for n workers: 1 + 6n + 2 nnz int32 values.
-size_t plan_stage_bytes(int n) { return sizeof(int32_t) * (1 + 6 * static_cast<size_t>(n) + 2 * n * n); }
+// Largest visit plan (plan.cpp) for n workers: at most n super-steps of 2
+// header values, n new z values (2 each) and n rows (3 + 2 per entry), so
+// 1 + 7n + 2 nnz int32 values with nnz <= n*n.
+size_t plan_stage_bytes(int n) { return sizeof(int32_t) * (1 + 7 * static_cast<size_t>(n) + 2 * n * n); }
 
 size_t stage_bytes(int n) { return std::max(csr_stage_bytes(n), plan_stage_bytes(n)); }
 
@@ -250,6 +253,8 @@ gasloc_status upload_csr(gasloc_ctx* c, const int32_t* row_ptr, const int32_t* c
 
 // Copies a visit plan into the next pinned slot and enqueues its upload.
 gasloc_status upload_plan(gasloc_ctx* c, const std::vector<int32_t>& ops) {
+  if (sizeof(int32_t) * ops.size() > plan_stage_bytes(c->n))
+    return fail(c, GASLOC_EINVAL, "round plan larger than its staging buffer");
   const int slot = c->stage_next;
   c->stage_next = (c->stage_next + 1) % kStageSlots;
   if (c->stage_used[slot]) HIP_TRY(c, hipEventSynchronize(c->stage_done[slot]));
@@ -374,15 +379,23 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
   bool planned = false;
   int slots = 0;
   if (c->hp.round_form == GASLOC_FORM_EQ) {
+    // super-steps of as many new z values as the kernel batches loads for
     std::string err;
-    if (!gasloc::plan_round(c->n, rp, col, val, &c->plan_ops, &slots, &err)) return fail(c, GASLOC_EINVAL, err);
+    if (!gasloc::plan_round(c->n, rp, col, val, kPlanBatch, gasloc::kPlanRows, &c->plan_ops, &slots, &err))
+      return fail(c, GASLOC_EINVAL, err);
     planned = use_planned(*c, slots);
   }
   gasloc::LaunchShape shape;
   size_t lds = 0;
   if (planned) {
     const int ops_len = static_cast<int>(c->plan_ops.size());
-    shape = gasloc::LaunchShape{4, 256, 0, 4};
+    // 4 columns per thread when the plan needs few slots (n=64 1-Peer: 10.65
+    // ms); with many slots 2 columns, whose lower register use keeps more
+    // waves per CU (n=32 3-regular bf16: 23.3-24.0 ms vs 28.7-29.6 ms with 4);
+    // 1 if a 256-thread workgroup would use more than a quarter of a CU's LDS
+    shape = gasloc::LaunchShape{slots <= 8 ? 4 : 2, 256, 0, kPlanBatch};
+    if (gasloc::planned_lds_bytes(slots, ops_len, shape) + gasloc::kStaticLds > c->lds_per_cu / 4) shape.vec = 2;
+    if (gasloc::planned_lds_bytes(slots, ops_len, shape) + gasloc::kStaticLds > c->lds_per_cu / 4) shape.vec = 1;
     while (shape.threads > 64 && gasloc::planned_lds_bytes(slots, ops_len, shape) + gasloc::kStaticLds >
                                      std::min(c->lds_per_cu / 2, c->lds_per_block_max))
       shape.threads /= 2;
