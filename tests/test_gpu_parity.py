@@ -431,6 +431,27 @@ FULL = [
 ]
 
 
+def test_maximum_row_length_64bit_offsets():
+    # P = 2^31 - 1, the largest the ABI accepts: worker 1's row starts beyond
+    # element 2^31, so every kernel's element offsets exceed 32 bits, and the
+    # ragged last group of each row (P % 4 = 3) is exercised at the far end.
+    import torch
+
+    n, P = 2, (1 << 31) - 1
+    log("case max row length n=%d P=%d" % (n, P))
+    cols = gi.sample_columns(P, 1 << 12)
+    pair = Pair(n, P, "ring", "f32", gamma=0.1, cols=cols)
+    for t in range(2):
+        pair.local_step()
+        pair.local_step()
+        pair.gossip_round(t)
+        tail = pair.gpu.consensus_error_cols(P - 64, P)
+        reduction_close(tail, pair.oracles["f32"].consensus_error(slice(len(cols) - 64, len(cols))), "tail CE")
+    pair.check_state(tag="max row length")
+    del pair
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("name,sample,rounds", FULL)
 def test_full_size_sampled(name, sample, rounds):
     import torch
