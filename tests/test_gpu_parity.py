@@ -292,6 +292,32 @@ def test_explicit_nonsymmetric_csr_and_identity():
     pair.check_state(tag="explicit")
 
 
+@pytest.mark.parametrize("density", [0.05, 0.2, 0.6])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_explicit_random_csr_large_n(density, dtype):
+    # unstructured graphs at n = 40 (the slot-reusing kernel when the plan
+    # reuses slots), some rows without their own entry
+    n, P = 40, 20_011
+    rng = np.random.default_rng(int(density * 100) + (dtype == "bf16"))
+    pair = Pair(n, P, "ring", dtype, gamma=0.1)
+    for t in range(3):
+        pair.local_step()
+        dense = rng.random((n, n)) * (rng.random((n, n)) < density)
+        dense[np.arange(n), np.arange(n)] = (rng.random(n) < 0.8) * rng.random(n)
+        dense[dense.sum(axis=1) == 0, 0] = 1.0
+        dense /= dense.sum(axis=1, keepdims=True)
+        rp = np.zeros(n + 1, np.int32)
+        cols, vals = [], []
+        for i in range(n):
+            nz = np.nonzero(dense[i])[0]
+            cols += nz.tolist()
+            vals += dense[i, nz].tolist()
+            rp[i + 1] = len(cols)
+        pair.gossip_round(t, W=(rp, np.array(cols, np.int32), np.array(vals, np.float32)))
+        reduction_close(pair.gpu.consensus_error(), pair.oracles["f32"].consensus_error(), "CE round %d" % t)
+    pair.check_state(tag="explicit n=40 density %g" % density)
+
+
 def test_all_inactive_step_changes_nothing():
     import torch
 
