@@ -17,13 +17,16 @@ constexpr int kMaxReplicas = 64;
 bool make_topology(const gasloc_topology& topo, int n, uint64_t t, int32_t* row_ptr, int32_t* col,
                    float* val, int32_t cap, int32_t* nnz, std::string* err);
 // Visit plan of a round for the slot-reusing kernel (plan.cpp): super-steps
-// of at most max_pre new z values and at most max_rows (<= kPlanRows) rows;
-// the plan is checked by verify_plan before it is returned.
+// of at most kPlanBatch new z values and at most kPlanRows rows; the plan is
+// checked by verify_plan before it is returned.
+constexpr int kPlanBatch = 4;
 constexpr int kPlanRows = 4;
-bool plan_round(int n, const int32_t* rp, const int32_t* col, const float* val, int max_pre, int max_rows,
-                std::vector<int32_t>* ops, int* slots_used, std::string* err);
+bool plan_round(int n, const int32_t* rp, const int32_t* col, const float* val, std::vector<int32_t>* ops,
+                int* slots_used, std::string* err);
 bool verify_plan(int n, const int32_t* rp, const int32_t* col, const float* val, const int32_t* ops, int len,
-                 int slots, int max_rows, std::string* err);
+                 int slots, std::string* err);
+// Upper bound on the words of a plan for n workers.
+size_t plan_words_max(int n);
 bool skip_exchanges(int n, const int32_t* rp, const int32_t* col, const float* val, const uint8_t* alive,
                     const uint8_t* link_ok, int32_t* out_rp, int32_t* out_col, float* out_val, int32_t cap,
                     int32_t* nnz, std::string* err);
@@ -72,7 +75,6 @@ struct GossipArgs {
 
   // planned visit order (k_gossip_planned only): see plan.cpp
   const int32_t* ops;
-  int32_t ops_len;
   int32_t slots;
 
   // Fused last local step (the fused kernel only): every worker i with bit i
@@ -102,7 +104,8 @@ hipError_t launch_gossip_round(const GossipArgs& a, int dtype, bool fused, int f
                                const LaunchShape& shape, hipStream_t stream);
 hipError_t launch_gossip_planned(const GossipArgs& a, int dtype, bool fused, const LaunchShape& shape,
                                  hipStream_t stream);
-size_t planned_lds_bytes(int slots, int ops_len, const LaunchShape& shape);
+// Dynamic LDS bytes of one workgroup of the planned kernel (z slots only).
+size_t planned_lds_bytes(int slots, const LaunchShape& shape);
 hipError_t launch_consensus_error(const void* x, int dtype, int64_t ld, int n, int64_t p_begin,
                                   int64_t p_end, double* partials, int blocks, hipStream_t stream);
 hipError_t launch_finalize(const double* partials, int count, double* out, hipStream_t stream);

@@ -491,157 +491,336 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// The EQ round with a host-planned visit order (plan.cpp): each super-step
-// computes the z of the workers first read by its rows into free LDS slots
-// (loads of up to R workers and the rows' zp in flight together), then emits
-// up to kPlanRows rows.  LDS holds `slots` values per column instead of n, so sparse
-// graphs keep many more columns in flight per CU.  Per element the
-// arithmetic is exactly that of k_gossip_round<..., GASLOC_FORM_EQ>.
+// The EQ round with a host-planned visit order (plan.cpp).  Each super-step
+// computes the z of the workers its rows read first (at most R of them) into
+// free LDS slots, then emits up to kPlanRows rows.  LDS holds `slots` values
+// per column instead of n, so sparse graphs keep many more columns in flight
+// per CU.  Per element the arithmetic is exactly that of
+// k_gossip_round<..., GASLOC_FORM_EQ>.
+//
+// The plan is the same for every column, so it is read through the scalar
+// cache (constant address space): worker and slot indices, counts and weights
+// are wave-uniform and all control flow is scalar.  The loads of the next
+// super-step (of this column group, or the first of the next group) are issued
+// before the current one is computed, so a wave keeps one super-step of
+// operands in flight while it works; they are held as raw words and decoded at
+// their use, which keeps the loads outstanding until then.
+//
+// Plan words: [S, start_0 .. start_{S-1}], super-step at start_s:
+//   npre, nrows, (worker, slot) x npre, row x nrows,
+//   then per row: nent, own_slot, (slot, weight bits) x nent.
 // ---------------------------------------------------------------------------
+
+typedef const __attribute__((address_space(4))) int32_t plan_word;
+
+// 32-bit words holding V values of dtype DT as stored
+template <int DT, int V>
+struct RawWords {
+  static constexpr int count = DT == GASLOC_BF16 ? (V + 1) / 2 : V;
+};
+
+template <int DT, int V>
+__device__ __forceinline__ void load_raw(const void* base, int64_t idx, int cnt,
+                                         uint32_t (&w)[RawWords<DT, V>::count]) {
+  if constexpr (DT == GASLOC_BF16) {
+    const uint16_t* p = static_cast<const uint16_t*>(base) + idx;
+    if (cnt == V) {
+      if constexpr (V == 4) {
+        const u32x2 t = ld_stream(reinterpret_cast<const u32x2*>(p));
+        w[0] = t.x;
+        w[1] = t.y;
+      } else if constexpr (V == 2) {
+        w[0] = ld_stream(reinterpret_cast<const uint32_t*>(p));
+      } else {
+        w[0] = *p;
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < RawWords<DT, V>::count; ++k) w[k] = 0u;
+#pragma unroll
+      for (int c = 0; c < V; ++c)
+        if (c < cnt) w[c / 2] |= static_cast<uint32_t>(p[c]) << (16 * (c & 1));
+    }
+  } else {
+    const float* p = static_cast<const float*>(base) + idx;
+    if (cnt == V) {
+      if constexpr (V == 4) {
+        const f32x4 t = ld_stream(reinterpret_cast<const f32x4*>(p));
+        w[0] = __float_as_uint(t.x);
+        w[1] = __float_as_uint(t.y);
+        w[2] = __float_as_uint(t.z);
+        w[3] = __float_as_uint(t.w);
+      } else if constexpr (V == 2) {
+        const f32x2 t = ld_stream(reinterpret_cast<const f32x2*>(p));
+        w[0] = __float_as_uint(t.x);
+        w[1] = __float_as_uint(t.y);
+      } else {
+        w[0] = __float_as_uint(ld_stream(p));
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < V; ++c) w[c] = 0u;
+#pragma unroll
+      for (int c = 0; c < V; ++c)
+        if (c < cnt) w[c] = __float_as_uint(p[c]);
+    }
+  }
+}
+
+template <int DT, int V>
+__device__ __forceinline__ void decode_raw(const uint32_t (&w)[RawWords<DT, V>::count], float (&o)[V]) {
+#pragma unroll
+  for (int c = 0; c < V; ++c) {
+    if constexpr (DT == GASLOC_BF16)
+      o[c] = bf16_to_f32((w[c / 2] >> (16 * (c & 1))) & 0xffffu);
+    else
+      o[c] = __uint_as_float(w[c]);
+  }
+}
+
+// Operands of one super-step, loaded ahead of their use.  The fused AdamW
+// operands (g, m, v) are not staged: two super-steps of them would not fit
+// the register budget of the occupancy the LDS allows, so they are loaded
+// when the super-step is computed (with the next super-step's loads already
+// in flight).
+template <int DT, int V, int R>
+struct Staged {
+  static constexpr int PW = RawWords<DT, V>::count;
+  uint32_t x[R][PW], y[R][PW];
+  uint32_t u[R][V];
+  uint32_t zp[kPlanRows][V];
+};
+
+// TAIL: the workgroup's columns may run past P (per-thread cnt < V); else
+// every thread has V columns and the accesses need no per-lane branches.
+template <int DT, int V, int R, bool TAIL>
+__device__ __forceinline__ void planned_issue(const GossipArgs& a, plan_word* ops, int st, int64_t p, int cnt_tail,
+                                              Staged<DT, V, R>& b) {
+  const int cnt = TAIL ? cnt_tail : V;
+  const int at = ops[1 + st];
+  const int npre = ops[at], nrows = ops[at + 1];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (r >= npre) break;
+    const int j = ops[at + 2 + 2 * r];
+    const int64_t e = static_cast<int64_t>(j) * a.ld + p;
+    load_raw<DT, V>(a.x, e, cnt, b.x[r]);
+    if ((a.stepped >> j) & 1ull) load_raw<DT, V>(a.y, e, cnt, b.y[r]);
+    if (a.use_u) load_raw<GASLOC_F32, V>(a.u, e, cnt, b.u[r]);
+  }
+  if (a.apply_gamma) {
+    const int rows_at = at + 2 + 2 * npre;
+#pragma unroll
+    for (int rr = 0; rr < kPlanRows; ++rr) {
+      if (rr >= nrows) break;
+      load_raw<GASLOC_F32, V>(a.zp, static_cast<int64_t>(ops[rows_at + rr]) * a.ld + p, cnt, b.zp[rr]);
+    }
+  }
+}
+
+// Running consensus-error sums of one column group (shifted by its first
+// stored row, as in k_gossip_round); `fresh` until that row is stored.
+template <int V>
+struct CeSums {
+  double shift[V], s[V], q[V];
+  bool fresh;
+};
+
+template <int DT, int V, int R, bool FUSED, bool TAIL>
+__device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* ops, int st, int64_t p,
+                                                int cnt_tail, const Staged<DT, V, R>& b, float* mine,
+                                                int slot_stride, CeSums<V>& cs) {
+  const int cnt = TAIL ? cnt_tail : V;
+  const int at = ops[1 + st];
+  const int npre = ops[at], nrows = ops[at + 1];
+  if (st == 0) cs.fresh = true;
+  constexpr int RF = FUSED ? R : 1;
+  uint32_t gw[RF][V], mw[RF][V], vw[RF][V];
+  if constexpr (FUSED) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (r >= npre) break;
+      const int j = ops[at + 2 + 2 * r];
+      if ((a.active >> j) & 1ull) {
+        const int64_t e = static_cast<int64_t>(j) * a.ld + p;
+        load_raw<GASLOC_F32, V>(a.g, static_cast<int64_t>(j) * a.gld + p, cnt, gw[r]);
+        load_raw<GASLOC_F32, V>(a.m, e, cnt, mw[r]);
+        load_raw<GASLOC_F32, V>(a.v, e, cnt, vw[r]);
+      }
+    }
+  }
+  // post-outer iterates of the workers first read in this super-step
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (r >= npre) break;
+    const int j = ops[at + 2 + 2 * r];
+    const int slot = ops[at + 3 + 2 * r];
+    const int64_t e = static_cast<int64_t>(j) * a.ld + p;
+    float xv[V], yv[V], uv[V];
+    decode_raw<DT, V>(b.x[r], xv);
+    if ((a.stepped >> j) & 1ull) {
+      decode_raw<DT, V>(b.y[r], yv);
+    } else {
+#pragma unroll
+      for (int c = 0; c < V; ++c) yv[c] = xv[c];
+    }
+    if constexpr (FUSED) {
+      if ((a.active >> j) & 1ull) {
+        float gv[V], mv[V], vv[V];
+        decode_raw<GASLOC_F32, V>(gw[r], gv);
+        decode_raw<GASLOC_F32, V>(mw[r], mv);
+        decode_raw<GASLOC_F32, V>(vw[r], vv);
+        const float s1 = a.s1[j], c2 = a.c2[j];
+#pragma unroll
+        for (int c = 0; c < V; ++c)
+          yv[c] = as_stored<DT>(adamw_element(yv[c], gv[c], mv[c], vv[c], a.c_wd, a.b1, a.omb1, a.b2, a.omb2,
+                                              a.eps, s1, c2));
+        store_f32<V>(a.m + e, cnt, mv);
+        store_f32<V>(a.v + e, cnt, vv);
+      }
+    }
+    if (a.use_u) {
+      decode_raw<GASLOC_F32, V>(b.u[r], uv);
+    } else {
+#pragma unroll
+      for (int c = 0; c < V; ++c) uv[c] = 0.0f;
+    }
+    float* out = mine + slot * slot_stride;
+#pragma unroll
+    for (int c = 0; c < V; ++c) out[c] = outer_step(xv[c], xv[c] - yv[c], uv[c], a.mu, a.eta, a.nesterov);
+    if (a.use_u) store_f32<V>(a.u + e, cnt, uv);
+  }
+
+  // the rows: sum_k W_rk z_k in CSR order (+ gamma (z_r - zp_r)), zp_r = z_r
+  const int rows_at = at + 2 + 2 * npre;
+  int pos = rows_at + nrows;
+#pragma unroll
+  for (int rr = 0; rr < kPlanRows; ++rr) {
+    if (rr >= nrows) break;
+    const int row = ops[rows_at + rr];
+    const int nent = ops[pos];
+    const int own = ops[pos + 1];
+    const int64_t er = static_cast<int64_t>(row) * a.ld + p;
+    float acc[V];
+#pragma unroll
+    for (int c = 0; c < V; ++c) acc[c] = 0.0f;
+    // four entries' LDS reads in flight at a time, summed in CSR order
+    for (int k0 = 0; k0 < nent; k0 += 4) {
+      float zk[4][V], wk[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        if (k0 + t >= nent) break;
+        const float* src = mine + ops[pos + 2 + 2 * (k0 + t)] * slot_stride;
+        wk[t] = __int_as_float(ops[pos + 3 + 2 * (k0 + t)]);
+#pragma unroll
+        for (int c = 0; c < V; ++c) zk[t][c] = src[c];
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        if (k0 + t >= nent) break;
+#pragma unroll
+        for (int c = 0; c < V; ++c) acc[c] = acc[c] + wk[t] * zk[t][c];
+      }
+    }
+    pos += 2 + 2 * nent;
+    const float* zo = mine + own * slot_stride;
+    float zcur[V];
+#pragma unroll
+    for (int c = 0; c < V; ++c) zcur[c] = zo[c];
+    if (a.apply_gamma) {
+      float zpv[V];
+      decode_raw<GASLOC_F32, V>(b.zp[rr], zpv);
+#pragma unroll
+      for (int c = 0; c < V; ++c) acc[c] = acc[c] + a.gamma * (zcur[c] - zpv[c]);
+    }
+    if (a.store_zp) store_f32<V>(a.zp + er, cnt, zcur);
+    float kept[V];
+    store_params<DT, V>(a.x, er, cnt, acc, kept);
+#pragma unroll
+    for (int c = 0; c < V; ++c) {
+      const double xd = static_cast<double>(kept[c]);
+      if (cs.fresh) {
+        cs.shift[c] = xd;
+        cs.s[c] = 0.0;
+        cs.q[c] = 0.0;
+      }
+      const double dv = xd - cs.shift[c];
+      cs.s[c] += dv;
+      cs.q[c] += dv * dv;
+    }
+    cs.fresh = false;
+  }
+}
 
 template <int DT, int V, int R, bool FUSED>
 __global__ __launch_bounds__(256) void k_gossip_planned(GossipArgs a) {
-  extern __shared__ __align__(16) unsigned char lds[];
+  extern __shared__ __align__(16) float zs[];  // [slots][nt][V]
+  plan_word* ops = (plan_word*)(a.ops);  // address-space cast: read-only for the whole launch
   const int nt = blockDim.x;
   const int tid = threadIdx.x;
-  float* zs = reinterpret_cast<float*>(lds);  // [slots][nt][V]
-  int32_t* ops = reinterpret_cast<int32_t*>(lds + static_cast<size_t>(a.slots) * nt * V * sizeof(float));
-  for (int k = tid; k < a.ops_len; k += nt) ops[k] = a.ops[k];
-  __syncthreads();
-
-  const double inv_n = 1.0 / static_cast<double>(a.n);
   const int steps = ops[0];
+  const double inv_n = 1.0 / static_cast<double>(a.n);
+  const int slot_stride = nt * V;
+  float* mine = zs + tid * V;
+
+  // column groups blockIdx.x * nt + it * (gridDim.x * nt) + tid, it < iters:
+  // the same count for every thread of the workgroup, so control stays
+  // uniform.  Every iteration but possibly the last gives each thread V
+  // columns; in that last one threads past P see cnt < V (0 beyond the end)
   const int64_t groups = (a.P + V - 1) / V;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * nt;
+  const int64_t whole = a.P / V;  // groups with V columns
+  const int64_t span = static_cast<int64_t>(gridDim.x) * nt;
+  const int64_t first = static_cast<int64_t>(blockIdx.x) * nt;
+  const int64_t iters = first < groups ? (groups - first + span - 1) / span : 0;
+  const int64_t full_iters =
+      first + nt <= whole ? (iters < (whole - first - nt) / span + 1 ? iters : (whole - first - nt) / span + 1) : 0;
+  auto column = [&](int64_t it) { return (first + it * span + tid) * V; };
+
+  Staged<DT, V, R> A, B;
+  CeSums<V> cs;
   double ce = 0.0;
-  for (int64_t gi = static_cast<int64_t>(blockIdx.x) * nt + tid; gi < groups; gi += stride) {
-    const int64_t p = gi * V;
-    const int cnt = static_cast<int>(a.P - p < V ? a.P - p : V);
-    auto slot = [&](int s) { return zs + (static_cast<size_t>(s) * nt + tid) * V; };
-    double shift[V], s[V], q[V];
-    bool first_row = true;
-    int pc = 1;
+  int64_t it_issue = 0, it_use = 0;
+  int st_issue = 0, st_use = 0;
+  auto issue = [&](Staged<DT, V, R>& b) {
+    planned_issue<DT, V, R, false>(a, ops, st_issue, column(it_issue), V, b);
+    if (++st_issue == steps) {
+      st_issue = 0;
+      ++it_issue;
+    }
+  };
+  auto use = [&](const Staged<DT, V, R>& b) {
+    planned_consume<DT, V, R, FUSED, false>(a, ops, st_use, column(it_use), V, b, mine, slot_stride, cs);
+    if (++st_use == steps) {
+#pragma unroll
+      for (int c = 0; c < V; ++c) ce += cs.q[c] - cs.s[c] * cs.s[c] * inv_n;
+      st_use = 0;
+      ++it_use;
+    }
+  };
+  // two super-steps per trip, alternating the operand buffers
+  const int64_t total = full_iters * steps;
+  if (total > 0) issue(A);
+  for (int64_t k = 0; k < total; k += 2) {
+    if (k + 1 < total) issue(B);
+    use(A);
+    if (k + 1 >= total) break;
+    if (k + 2 < total) issue(A);
+    use(B);
+  }
+  if (full_iters < iters) {  // the ragged last iteration, not pipelined
+    const int64_t col = column(full_iters);
+    const int64_t left = a.P - col;
+    const int cnt = left >= V ? V : (left > 0 ? static_cast<int>(left) : 0);
     for (int st = 0; st < steps; ++st) {
-      const int npre = ops[pc];
-      const int pre = pc + 1;
-      int rq = pre + 2 * npre;
-      const int nrows = ops[rq++];
-      // the consensus-momentum reads of this super-step's rows go out first
-      int rowpos[kPlanRows];
-      float zpv[kPlanRows][V];
-#pragma unroll
-      for (int rr = 0; rr < kPlanRows; ++rr) {
-        if (rr >= nrows) break;
-        rowpos[rr] = rq;
-        if (a.apply_gamma) load_f32<V>(a.zp + static_cast<int64_t>(ops[rq]) * a.ld + p, cnt, zpv[rr]);
-        rq += 3 + 2 * ops[rq + 1];
-      }
-      pc = rq;
-
-      // post-outer iterates of the workers first read in this super-step
-      for (int q0 = 0; q0 < npre; q0 += R) {
-        constexpr int RF = FUSED ? R : 1;
-        float xv[R][V], yv[R][V], uv[R][V];
-        float gv[RF][V], mv[RF][V], vv[RF][V];
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-          if (q0 + r >= npre) break;
-          const int j = ops[pre + 2 * (q0 + r)];
-          const int64_t e = static_cast<int64_t>(j) * a.ld + p;
-          load_params<DT, V>(a.x, e, cnt, xv[r]);
-          if ((a.stepped >> j) & 1ull) {
-            load_params<DT, V>(a.y, e, cnt, yv[r]);
-          } else {
-#pragma unroll
-            for (int c = 0; c < V; ++c) yv[r][c] = xv[r][c];
-          }
-          if constexpr (FUSED) {
-            if ((a.active >> j) & 1ull) {
-              load_f32<V>(a.g + static_cast<int64_t>(j) * a.gld + p, cnt, gv[r]);
-              load_f32<V>(a.m + e, cnt, mv[r]);
-              load_f32<V>(a.v + e, cnt, vv[r]);
-            }
-          }
-          if (a.use_u) {
-            load_f32<V>(a.u + e, cnt, uv[r]);
-          } else {
-#pragma unroll
-            for (int c = 0; c < V; ++c) uv[r][c] = 0.0f;
-          }
-        }
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-          if (q0 + r >= npre) break;
-          const int j = ops[pre + 2 * (q0 + r)];
-          const int64_t e = static_cast<int64_t>(j) * a.ld + p;
-          if constexpr (FUSED) {
-            if ((a.active >> j) & 1ull) {
-              const float s1 = a.s1[j], c2 = a.c2[j];
-#pragma unroll
-              for (int c = 0; c < V; ++c)
-                yv[r][c] = as_stored<DT>(adamw_element(yv[r][c], gv[r][c], mv[r][c], vv[r][c], a.c_wd, a.b1,
-                                                       a.omb1, a.b2, a.omb2, a.eps, s1, c2));
-              store_f32<V>(a.m + e, cnt, mv[r]);
-              store_f32<V>(a.v + e, cnt, vv[r]);
-            }
-          }
-          float* out = slot(ops[pre + 2 * (q0 + r) + 1]);
-#pragma unroll
-          for (int c = 0; c < V; ++c)
-            out[c] = outer_step(xv[r][c], xv[r][c] - yv[r][c], uv[r][c], a.mu, a.eta, a.nesterov);
-          if (a.use_u) store_f32<V>(a.u + e, cnt, uv[r]);
-        }
-      }
-
-      // the rows: sum_k W_rk z_k in CSR order (+ gamma (z_r - zp_r)), zp_r = z_r
-#pragma unroll
-      for (int rr = 0; rr < kPlanRows; ++rr) {
-        if (rr >= nrows) break;
-        const int at = rowpos[rr];
-        const int row = ops[at];
-        const int nent = ops[at + 1];
-        const int64_t er = static_cast<int64_t>(row) * a.ld + p;
-        float acc[V];
-#pragma unroll
-        for (int c = 0; c < V; ++c) acc[c] = 0.0f;
-        for (int kk = 0; kk < nent; ++kk) {
-          const float* zk = slot(ops[at + 2 + 2 * kk]);
-          const float w = __int_as_float(ops[at + 3 + 2 * kk]);
-#pragma unroll
-          for (int c = 0; c < V; ++c) acc[c] = acc[c] + w * zk[c];
-        }
-        const float* zo = slot(ops[at + 2 + 2 * nent]);
-        float zcur[V];
-#pragma unroll
-        for (int c = 0; c < V; ++c) zcur[c] = zo[c];
-        if (a.apply_gamma) {
-#pragma unroll
-          for (int c = 0; c < V; ++c) acc[c] = acc[c] + a.gamma * (zcur[c] - zpv[rr][c]);
-        }
-        if (a.store_zp) store_f32<V>(a.zp + er, cnt, zcur);
-        float kept[V];
-        store_params<DT, V>(a.x, er, cnt, acc, kept);
-#pragma unroll
-        for (int c = 0; c < V; ++c) {
-          const double xd = static_cast<double>(kept[c]);
-          if (first_row) {
-            shift[c] = xd;
-            s[c] = 0.0;
-            q[c] = 0.0;
-          }
-          const double dv = xd - shift[c];
-          s[c] += dv;
-          q[c] += dv * dv;
-        }
-        first_row = false;
-      }
+      planned_issue<DT, V, R, true>(a, ops, st, col, cnt, A);
+      planned_consume<DT, V, R, FUSED, true>(a, ops, st, col, cnt, A, mine, slot_stride, cs);
     }
 #pragma unroll
     for (int c = 0; c < V; ++c)
-      if (c < cnt) ce += q[c] - s[c] * s[c] * inv_n;
+      if (c < cnt) ce += cs.q[c] - cs.s[c] * cs.s[c] * inv_n;
   }
-  const double total = block_sum(ce);
-  if (tid == 0) a.partials[blockIdx.x] = total;
+  const double block_total = block_sum(ce);
+  if (tid == 0) a.partials[blockIdx.x] = block_total;
 }
 
 // ---------------------------------------------------------------------------
@@ -765,17 +944,14 @@ hipError_t launch_local_adamw(const AdamArgs& a, int dtype, int blocks_per_worke
   return hipGetLastError();
 }
 
-size_t planned_lds_bytes(int slots, int ops_len, const LaunchShape& s) {
-  return static_cast<size_t>(slots) * s.threads * s.vec * sizeof(float) + static_cast<size_t>(ops_len) * 4;
+size_t planned_lds_bytes(int slots, const LaunchShape& s) {
+  return static_cast<size_t>(slots) * s.threads * s.vec * sizeof(float);
 }
 
 template <int DT, int V, bool FUSED>
 hipError_t launch_planned_typed(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
-  const size_t lds = planned_lds_bytes(a.slots, a.ops_len, s);
-  if (s.batch <= 2)
-    hipLaunchKernelGGL((k_gossip_planned<DT, V, 2, FUSED>), dim3(s.blocks), dim3(s.threads), lds, stream, a);
-  else
-    hipLaunchKernelGGL((k_gossip_planned<DT, V, 4, FUSED>), dim3(s.blocks), dim3(s.threads), lds, stream, a);
+  hipLaunchKernelGGL((k_gossip_planned<DT, V, kPlanBatch, FUSED>), dim3(s.blocks), dim3(s.threads),
+                     planned_lds_bytes(a.slots, s), stream, a);
   return hipGetLastError();
 }
 

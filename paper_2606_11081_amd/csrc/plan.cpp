@@ -6,15 +6,15 @@
 // flight per CU by LDS / (4 n) bytes.  The plan instead emits rows in an order
 // that computes each z_j just before its first reader and frees its LDS slot
 // after its last reader, so a sparse W needs only a few slots.  Rows are
-// grouped into super-steps: the z of up to `max_pre` workers are computed
-// together (their loads in flight at once), then up to `max_rows` rows are
+// grouped into super-steps: the z of up to kPlanBatch workers are computed
+// together (their loads in flight at once), then up to kPlanRows rows are
 // emitted.  The per-row arithmetic, including the ascending-column summation
 // order of every row, is that of the phase kernel; only independent work is
 // reordered.
 //
-// Encoding (int32): [super-steps] then per super-step
-//   n_pre, (worker, slot) x n_pre,
-//   n_rows, per row: row, n_ent, (slot, weight bits) x n_ent, own_slot
+// Encoding (int32): [S, start_0 .. start_{S-1}], and at start_s super-step s:
+//   n_pre, n_rows, (worker, slot) x n_pre, row x n_rows,
+//   then per row: n_ent, own_slot, (slot, weight bits) x n_ent
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
@@ -25,8 +25,12 @@
 
 namespace gasloc {
 
-bool plan_round(int n, const int32_t* rp, const int32_t* col, const float* val, int max_pre, int max_rows,
-                std::vector<int32_t>* ops, int* slots_used, std::string* err) {
+namespace {
+
+// One greedy plan starting from row `first`.
+void greedy_plan(int n, const int32_t* rp, const int32_t* col, const float* val, int first,
+                 std::vector<int32_t>* ops, int* slots_used) {
+  constexpr int max_pre = kPlanBatch, max_rows = kPlanRows;
   // need[i]: columns of row i plus i itself, ascending
   std::vector<std::vector<int>> need(static_cast<size_t>(n));
   std::vector<int> uses(static_cast<size_t>(n), 0);
@@ -41,30 +45,38 @@ bool plan_round(int n, const int32_t* rp, const int32_t* col, const float* val, 
   std::vector<int> slot_of(static_cast<size_t>(n), -1);
   std::vector<char> emitted(static_cast<size_t>(n), 0);
   std::vector<int> free_slots;  // sorted descending: back() is the lowest free slot
-  int high = 0, done = 0, supers = 0;
-  ops->clear();
-  ops->push_back(0);
+  int high = 0, done = 0;
+  std::vector<int32_t> body;
+  std::vector<int32_t> starts;
   std::vector<int> rows, pres;
   while (done < n) {
     rows.clear();
     pres.clear();
     for (;;) {
-      // next row: fewest new z to compute minus slots it frees; ties -> lowest index
-      int best = -1, best_cost = 1 << 30, best_new = 0;
+      // next row: fewest new z to compute minus slots it frees; ties -> the
+      // row with more of its z already live, then the lowest index
+      int best = -1, best_cost = 1 << 30, best_new = 0, best_live = -1;
       for (int i = 0; i < n; ++i) {
         if (emitted[static_cast<size_t>(i)]) continue;
-        int cost = 0, fresh = 0;
+        int cost = 0, fresh = 0, live = 0;
         for (int j : need[static_cast<size_t>(i)]) {
           if (slot_of[static_cast<size_t>(j)] < 0) {
             ++cost;
             ++fresh;
+          } else {
+            ++live;
           }
           if (uses[static_cast<size_t>(j)] == 1) --cost;
         }
-        if (cost < best_cost) {
+        if (done == 0 && rows.empty()) {  // the first row is given
+          if (i != first) continue;
+          cost = -(1 << 29);
+        }
+        if (cost < best_cost || (cost == best_cost && live > best_live)) {
           best_cost = cost;
           best = i;
           best_new = fresh;
+          best_live = live;
         }
       }
       if (best < 0) break;
@@ -87,77 +99,124 @@ bool plan_round(int n, const int32_t* rp, const int32_t* col, const float* val, 
       emitted[static_cast<size_t>(best)] = 1;
       ++done;
     }
-    ops->push_back(static_cast<int32_t>(pres.size()));
-    for (int j : pres) {
-      ops->push_back(j);
-      ops->push_back(slot_of[static_cast<size_t>(j)]);
+    // a row that alone needs more than kPlanBatch new z values gets super-steps
+    // of its first values with no rows before it
+    size_t q = 0;
+    while (pres.size() - q > static_cast<size_t>(max_pre)) {
+      starts.push_back(static_cast<int32_t>(body.size()));
+      body.push_back(max_pre);
+      body.push_back(0);
+      for (int k = 0; k < max_pre; ++k, ++q) {
+        body.push_back(pres[q]);
+        body.push_back(slot_of[static_cast<size_t>(pres[q])]);
+      }
     }
-    ops->push_back(static_cast<int32_t>(rows.size()));
+    starts.push_back(static_cast<int32_t>(body.size()));
+    body.push_back(static_cast<int32_t>(pres.size() - q));
+    body.push_back(static_cast<int32_t>(rows.size()));
+    for (; q < pres.size(); ++q) {
+      body.push_back(pres[q]);
+      body.push_back(slot_of[static_cast<size_t>(pres[q])]);
+    }
+    for (int r : rows) body.push_back(r);
     for (int r : rows) {
-      ops->push_back(r);
-      ops->push_back(rp[r + 1] - rp[r]);
+      body.push_back(rp[r + 1] - rp[r]);
+      body.push_back(slot_of[static_cast<size_t>(r)]);
       for (int32_t k = rp[r]; k < rp[r + 1]; ++k) {
         int32_t bits;
         std::memcpy(&bits, &val[k], sizeof bits);
-        ops->push_back(slot_of[static_cast<size_t>(col[k])]);
-        ops->push_back(bits);
+        body.push_back(slot_of[static_cast<size_t>(col[k])]);
+        body.push_back(bits);
       }
-      ops->push_back(slot_of[static_cast<size_t>(r)]);
     }
     // slots are released only after the whole super-step has been emitted
     for (int r : rows)
       for (int j : need[static_cast<size_t>(r)])
         if (--uses[static_cast<size_t>(j)] == 0) free_slots.push_back(slot_of[static_cast<size_t>(j)]);
     std::sort(free_slots.begin(), free_slots.end(), std::greater<int>());
-    ++supers;
   }
-  (*ops)[0] = supers;
+  const int32_t supers = static_cast<int32_t>(starts.size());
+  ops->assign(1, supers);
+  for (int32_t at : starts) ops->push_back(1 + supers + at);
+  ops->insert(ops->end(), body.begin(), body.end());
   *slots_used = high;
-  return verify_plan(n, rp, col, val, ops->data(), static_cast<int>(ops->size()), high, max_rows, err);
 }
 
-// Replays a plan symbolically: every slot read holds the worker the CSR
-// names, every z is computed exactly once before use, every row is emitted
-// exactly once with its CSR entries in order, slots stay within `slots`,
-// super-steps hold at most max_rows rows.
+}  // namespace
+
+size_t plan_words_max(int n) {
+  // S <= n + n / kPlanBatch <= 2 n super-steps: 1 + S starts, 2 S counts,
+  // 2 n pre words, n row ids, 2 n row headers and 2 nnz <= 2 n^2 entry words
+  const size_t m = static_cast<size_t>(n);
+  return 1 + 6 * m + 5 * m + 2 * m * m;
+}
+
+bool plan_round(int n, const int32_t* rp, const int32_t* col, const float* val, std::vector<int32_t>* ops,
+                int* slots_used, std::string* err) {
+  greedy_plan(n, rp, col, val, 0, ops, slots_used);
+  // graphs with many live values at once: try a few other first rows and
+  // keep the plan that needs the fewest slots (deterministic choice)
+  if (*slots_used > 8) {
+    std::vector<int32_t> trial;
+    int trial_slots = 0;
+    const int tries = std::min(n, 8);
+    for (int t = 1; t < tries; ++t) {
+      greedy_plan(n, rp, col, val, t * n / tries, &trial, &trial_slots);
+      if (trial_slots < *slots_used) {
+        ops->swap(trial);
+        *slots_used = trial_slots;
+      }
+    }
+  }
+  return verify_plan(n, rp, col, val, ops->data(), static_cast<int>(ops->size()), *slots_used, err);
+}
+
+// Replays a plan symbolically: the start table points at consecutive
+// super-steps that tile the words after it; every slot read holds the worker
+// the CSR names; every z is computed exactly once before use; every row is
+// emitted exactly once with its CSR entries in order; slots stay within
+// `slots`; super-steps hold at most kPlanRows rows and kPlanBatch new z, and
+// a super-step without rows is followed by one that has some.
 bool verify_plan(int n, const int32_t* rp, const int32_t* col, const float* val, const int32_t* ops, int len,
-                 int slots, int max_rows, std::string* err) {
+                 int slots, std::string* err) {
   auto bad = [&](const char* what) {
     *err = std::string("round plan: ") + what;
     return false;
   };
-  if (len < 1 || ops[0] < 1 || ops[0] > n) return bad("super-step count");
+  if (len < 1 || ops[0] < 1 || ops[0] > 2 * n || len < 1 + ops[0]) return bad("super-step count");
+  const int supers = ops[0];
   std::vector<int> holder(static_cast<size_t>(slots), -1);
   std::vector<char> computed(static_cast<size_t>(n), 0), emitted(static_cast<size_t>(n), 0);
-  int pc = 1, rows_seen = 0;
-  for (int s = 0; s < ops[0]; ++s) {
-    if (pc >= len) return bad("truncated");
-    const int npre = ops[pc++];
-    if (npre < 0 || pc + 2 * npre + 1 > len) return bad("pre count");
+  int pc = 1 + supers, rows_seen = 0;
+  for (int s = 0; s < supers; ++s) {
+    if (ops[1 + s] != pc || pc + 2 > len) return bad("super-step start");
+    const int npre = ops[pc], nrows = ops[pc + 1];
+    pc += 2;
+    if (npre < 0 || npre > kPlanBatch || nrows < 0 || nrows > kPlanRows || npre + nrows == 0 ||
+        (nrows == 0 && s == supers - 1) || pc + 2 * npre + nrows > len)
+      return bad("super-step counts");
     for (int q = 0; q < npre; ++q) {
       const int j = ops[pc++], slot = ops[pc++];
       if (j < 0 || j >= n || computed[static_cast<size_t>(j)] || slot < 0 || slot >= slots) return bad("pre");
       computed[static_cast<size_t>(j)] = 1;
       holder[static_cast<size_t>(slot)] = j;
     }
-    const int nrows = ops[pc++];
-    if (nrows < 1 || nrows > max_rows) return bad("row count");
+    const int ids = pc;
+    pc += nrows;
     for (int q = 0; q < nrows; ++q) {
-      if (pc + 2 > len) return bad("truncated row");
-      const int r = ops[pc++], nent = ops[pc++];
-      if (r < 0 || r >= n || emitted[static_cast<size_t>(r)] || nent != rp[r + 1] - rp[r] ||
-          pc + 2 * nent + 1 > len)
-        return bad("row header");
+      const int r = ops[ids + q];
+      if (r < 0 || r >= n || emitted[static_cast<size_t>(r)] || pc + 2 > len) return bad("row id");
+      const int nent = ops[pc], own = ops[pc + 1];
+      pc += 2;
+      if (nent != rp[r + 1] - rp[r] || pc + 2 * nent > len) return bad("row header");
+      if (own < 0 || own >= slots || holder[static_cast<size_t>(own)] != r) return bad("own slot");
       for (int e = 0; e < nent; ++e) {
         const int slot = ops[pc++];
         int32_t bits;
         std::memcpy(&bits, &val[rp[r] + e], sizeof bits);
-        if (slot < 0 || slot >= slots || holder[static_cast<size_t>(slot)] != col[rp[r] + e] ||
-            ops[pc++] != bits)
+        if (slot < 0 || slot >= slots || holder[static_cast<size_t>(slot)] != col[rp[r] + e] || ops[pc++] != bits)
           return bad("entry");
       }
-      const int own = ops[pc++];
-      if (own < 0 || own >= slots || holder[static_cast<size_t>(own)] != r) return bad("own slot");
       emitted[static_cast<size_t>(r)] = 1;
       ++rows_seen;
     }

@@ -21,7 +21,6 @@ using gasloc::kMaxReplicas;
 namespace {
 
 constexpr int kStageSlots = 4;      // pinned CSR staging slots, reused round-robin
-constexpr int kPlanBatch = 4;       // new z values per super-step of a round plan
 constexpr int kMaxGridBlocks = 16384;
 
 thread_local std::string g_thread_error;
@@ -44,10 +43,8 @@ size_t csr_stage_bytes(int n) {
   return sizeof(int32_t) * static_cast<size_t>(n + 1) + (sizeof(int32_t) + sizeof(float)) * n * n;
 }
 
-// Largest visit plan (plan.cpp) for n workers: at most n super-steps of 2
-// header values, n new z values (2 each) and n rows (3 + 2 per entry), so
-// 1 + 7n + 2 nnz int32 values with nnz <= n*n.
-size_t plan_stage_bytes(int n) { return sizeof(int32_t) * (1 + 7 * static_cast<size_t>(n) + 2 * n * n); }
+// Largest visit plan (plan.cpp) for n workers.
+size_t plan_stage_bytes(int n) { return sizeof(int32_t) * gasloc::plan_words_max(n); }
 
 size_t stage_bytes(int n) { return std::max(csr_stage_bytes(n), plan_stage_bytes(n)); }
 
@@ -268,7 +265,7 @@ gasloc_status upload_plan(gasloc_ctx* c, const std::vector<int32_t>& ops) {
 
 // Which EQ-form kernel runs a round: the phase kernel keeps every worker's z
 // in LDS; the planned kernel (plan.cpp) keeps only the live ones.  Measured
-// on MI355X: planned is 2.3x faster at n=64 (1-Peer) and 1.4x at n=32
+// on MI355X: planned is 2.3x faster at n=64 (1-Peer) and 1.9x at n=32
 // (3-regular), where LDS limits the phase kernel; at n <= 16 the phase
 // kernel fits and keeps more loads in flight (fused round at n=16: 45.0 vs
 // 48.2 ms), and a dense W needs a slot per worker anyway.
@@ -381,26 +378,26 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
   if (c->hp.round_form == GASLOC_FORM_EQ) {
     // super-steps of as many new z values as the kernel batches loads for
     std::string err;
-    if (!gasloc::plan_round(c->n, rp, col, val, kPlanBatch, gasloc::kPlanRows, &c->plan_ops, &slots, &err))
+    if (!gasloc::plan_round(c->n, rp, col, val, &c->plan_ops, &slots, &err))
       return fail(c, GASLOC_EINVAL, err);
     planned = use_planned(*c, slots);
   }
   gasloc::LaunchShape shape;
   size_t lds = 0;
   if (planned) {
-    const int ops_len = static_cast<int>(c->plan_ops.size());
-    // 4 columns per thread when the plan needs few slots (n=64 1-Peer: 10.65
-    // ms); with many slots 2 columns, whose lower register use keeps more
-    // waves per CU (n=32 3-regular bf16: 23.3-24.0 ms vs 28.7-29.6 ms with 4);
-    // 1 if a 256-thread workgroup would use more than a quarter of a CU's LDS
-    shape = gasloc::LaunchShape{slots <= 8 ? 4 : 2, 256, 0, kPlanBatch};
-    if (gasloc::planned_lds_bytes(slots, ops_len, shape) + gasloc::kStaticLds > c->lds_per_cu / 4) shape.vec = 2;
-    if (gasloc::planned_lds_bytes(slots, ops_len, shape) + gasloc::kStaticLds > c->lds_per_cu / 4) shape.vec = 1;
-    while (shape.threads > 64 && gasloc::planned_lds_bytes(slots, ops_len, shape) + gasloc::kStaticLds >
+    // 4 columns per thread when the plan needs few slots (n=64 1-Peer: 10.7-
+    // 12.8 ms); with many slots 2 columns, so that four 256-thread workgroups
+    // fit a CU's LDS (n=32 3-regular bf16, 11-19 slots: 18.0-21.2 ms; 4
+    // columns in 128 threads measured the same); fewer columns, then fewer
+    // threads, while a workgroup would use more than a quarter of the LDS
+    shape = gasloc::LaunchShape{slots <= 8 ? 4 : 2, 256, 0, gasloc::kPlanBatch};
+    if (gasloc::planned_lds_bytes(slots, shape) + gasloc::kStaticLds > c->lds_per_cu / 4) shape.vec = 2;
+    if (gasloc::planned_lds_bytes(slots, shape) + gasloc::kStaticLds > c->lds_per_cu / 4) shape.vec = 1;
+    while (shape.threads > 64 && gasloc::planned_lds_bytes(slots, shape) + gasloc::kStaticLds >
                                      std::min(c->lds_per_cu / 2, c->lds_per_block_max))
       shape.threads /= 2;
     apply_shape_override(&shape);
-    lds = gasloc::planned_lds_bytes(slots, ops_len, shape) + gasloc::kStaticLds;
+    lds = gasloc::planned_lds_bytes(slots, shape) + gasloc::kStaticLds;
     const int per_cu = std::max(1, static_cast<int>(std::min<size_t>(c->lds_per_cu / lds, 8)));
     const int64_t needed = ((c->P + shape.vec - 1) / shape.vec + shape.threads - 1) / shape.threads;
     if (shape.blocks == 0)
@@ -458,7 +455,6 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
   a.partials = c->d_partials;
   if (planned) {
     a.ops = reinterpret_cast<const int32_t*>(c->d_csr);
-    a.ops_len = static_cast<int32_t>(c->plan_ops.size());
     a.slots = slots;
     HIP_TRY(c, gasloc::launch_gossip_planned(a, c->hp.param_dtype, step != nullptr, shape, c->stream));
   } else {

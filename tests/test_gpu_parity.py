@@ -132,7 +132,9 @@ def test_fused_last_step_matches_two_calls_and_oracle(n, P, topology, dtype, H, 
                 fused.local_step(active=act)
         split.gossip_round(t)
         ce_f, ce_s = fused.gpu.consensus_error(), split.gpu.consensus_error()
-        assert ce_f == ce_s
+        # the two launches may give a thread a different number of columns, which
+        # regroups the fp64 partial sums: equal up to the last bits
+        assert abs(ce_f - ce_s) <= 1e-12 * abs(ce_s)
         reduction_close(ce_f, fused.oracles["f32"].consensus_error(), "fused CE round %d" % t)
     torch.cuda.synchronize()
     for name in ("x", "m", "v", "u", "zp"):
