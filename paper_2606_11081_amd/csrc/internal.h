@@ -102,7 +102,7 @@ struct LaunchShape {
 hipError_t launch_local_adamw(const AdamArgs& a, int dtype, int blocks_per_worker, hipStream_t stream);
 hipError_t launch_gossip_round(const GossipArgs& a, int dtype, bool fused, int form,
                                const LaunchShape& shape, hipStream_t stream);
-hipError_t launch_gossip_planned(const GossipArgs& a, int dtype, bool fused, const LaunchShape& shape,
+hipError_t launch_gossip_planned(const GossipArgs& a, int dtype, bool fused, int form, const LaunchShape& shape,
                                  hipStream_t stream);
 // Dynamic LDS bytes of one workgroup of the planned kernel (z slots only).
 size_t planned_lds_bytes(int slots, const LaunchShape& shape);

@@ -578,24 +578,31 @@ __device__ __forceinline__ void decode_raw(const uint32_t (&w)[RawWords<DT, V>::
   }
 }
 
-// Operands of one super-step, loaded ahead of their use.  The fused AdamW
-// operands (g, m, v) are not staged: two super-steps of them would not fit
-// the register budget of the occupancy the LDS allows, so they are loaded
-// when the super-step is computed (with the next super-step's loads already
-// in flight).
+// Operands of one super-step, loaded ahead of their use:
+//   pa, pb, pu: the new slot workers' x, y, u (EQ); y or x (ALG1); x (the
+//               DAdam forms).  pb and pu are used by EQ only.
+//   ra, rf:     the rows' x (ALG1) or y (DAdam forms), and zp (EQ) or u
+//               (ALG1, Local-DAdam).
+// The fused AdamW operands (g, m, v) are not staged: two super-steps of them
+// would not fit the register budget of the occupancy the LDS allows, so they
+// are loaded when the super-step is computed (with the next super-step's
+// loads already in flight).
 template <int DT, int V, int R>
 struct Staged {
   static constexpr int PW = RawWords<DT, V>::count;
-  uint32_t x[R][PW], y[R][PW];
-  uint32_t u[R][V];
-  uint32_t zp[kPlanRows][V];
+  uint32_t pa[R][PW], pb[R][PW];
+  uint32_t pu[R][V];
+  uint32_t ra[kPlanRows][PW];
+  uint32_t rf[kPlanRows][V];
 };
 
 // TAIL: the workgroup's columns may run past P (per-thread cnt < V); else
 // every thread has V columns and the accesses need no per-lane branches.
-template <int DT, int V, int R, bool TAIL>
+template <int DT, int V, int R, int FORM, bool TAIL>
 __device__ __forceinline__ void planned_issue(const GossipArgs& a, plan_word* ops, int st, int64_t p, int cnt_tail,
                                               Staged<DT, V, R>& b) {
+  constexpr bool kEq = FORM == GASLOC_FORM_EQ;
+  constexpr bool kAlg1 = FORM == GASLOC_FORM_ALG1;
   const int cnt = TAIL ? cnt_tail : V;
   const int at = ops[1 + st];
   const int npre = ops[at], nrows = ops[at + 1];
@@ -604,16 +611,31 @@ __device__ __forceinline__ void planned_issue(const GossipArgs& a, plan_word* op
     if (r >= npre) break;
     const int j = ops[at + 2 + 2 * r];
     const int64_t e = static_cast<int64_t>(j) * a.ld + p;
-    load_raw<DT, V>(a.x, e, cnt, b.x[r]);
-    if ((a.stepped >> j) & 1ull) load_raw<DT, V>(a.y, e, cnt, b.y[r]);
-    if (a.use_u) load_raw<GASLOC_F32, V>(a.u, e, cnt, b.u[r]);
+    const bool stepped = (a.stepped >> j) & 1ull;
+    if constexpr (kEq) {
+      load_raw<DT, V>(a.x, e, cnt, b.pa[r]);
+      if (stepped) load_raw<DT, V>(a.y, e, cnt, b.pb[r]);
+      if (a.use_u) load_raw<GASLOC_F32, V>(a.u, e, cnt, b.pu[r]);
+    } else if constexpr (kAlg1) {
+      load_raw<DT, V>(stepped ? a.y : a.x, e, cnt, b.pa[r]);
+    } else {
+      load_raw<DT, V>(a.x, e, cnt, b.pa[r]);
+    }
   }
-  if (a.apply_gamma) {
-    const int rows_at = at + 2 + 2 * npre;
+  const int rows_at = at + 2 + 2 * npre;
 #pragma unroll
-    for (int rr = 0; rr < kPlanRows; ++rr) {
-      if (rr >= nrows) break;
-      load_raw<GASLOC_F32, V>(a.zp, static_cast<int64_t>(ops[rows_at + rr]) * a.ld + p, cnt, b.zp[rr]);
+  for (int rr = 0; rr < kPlanRows; ++rr) {
+    if (rr >= nrows) break;
+    const int row = ops[rows_at + rr];
+    const int64_t er = static_cast<int64_t>(row) * a.ld + p;
+    if constexpr (kEq) {
+      if (a.apply_gamma) load_raw<GASLOC_F32, V>(a.zp, er, cnt, b.rf[rr]);
+    } else if constexpr (kAlg1) {
+      load_raw<DT, V>(a.x, er, cnt, b.ra[rr]);
+      if (a.use_u) load_raw<GASLOC_F32, V>(a.u, er, cnt, b.rf[rr]);
+    } else {
+      if ((a.stepped >> row) & 1ull) load_raw<DT, V>(a.y, er, cnt, b.ra[rr]);
+      if (FORM == GASLOC_FORM_LOCAL_DADAM && a.use_u) load_raw<GASLOC_F32, V>(a.u, er, cnt, b.rf[rr]);
     }
   }
 }
@@ -626,10 +648,12 @@ struct CeSums {
   bool fresh;
 };
 
-template <int DT, int V, int R, bool FUSED, bool TAIL>
+template <int DT, int V, int R, bool FUSED, int FORM, bool TAIL>
 __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* ops, int st, int64_t p,
                                                 int cnt_tail, const Staged<DT, V, R>& b, float* mine,
                                                 int slot_stride, CeSums<V>& cs) {
+  constexpr bool kEq = FORM == GASLOC_FORM_EQ;
+  constexpr bool kAlg1 = FORM == GASLOC_FORM_ALG1;
   const int cnt = TAIL ? cnt_tail : V;
   const int at = ops[1 + st];
   const int npre = ops[at], nrows = ops[at + 1];
@@ -649,20 +673,27 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
       }
     }
   }
-  // post-outer iterates of the workers first read in this super-step
+  // slot values of the workers first read in this super-step: z (EQ), the
+  // live (fused: new) local iterate (ALG1), x (DAdam forms)
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     if (r >= npre) break;
     const int j = ops[at + 2 + 2 * r];
     const int slot = ops[at + 3 + 2 * r];
     const int64_t e = static_cast<int64_t>(j) * a.ld + p;
-    float xv[V], yv[V], uv[V];
-    decode_raw<DT, V>(b.x[r], xv);
-    if ((a.stepped >> j) & 1ull) {
-      decode_raw<DT, V>(b.y[r], yv);
-    } else {
+    const bool stepped = (a.stepped >> j) & 1ull;
+    float* out = mine + slot * slot_stride;
+    float xv[V], yv[V];
+    if constexpr (kEq) {
+      decode_raw<DT, V>(b.pa[r], xv);
+      if (stepped) {
+        decode_raw<DT, V>(b.pb[r], yv);
+      } else {
 #pragma unroll
-      for (int c = 0; c < V; ++c) yv[c] = xv[c];
+        for (int c = 0; c < V; ++c) yv[c] = xv[c];
+      }
+    } else {
+      decode_raw<DT, V>(b.pa[r], yv);  // ALG1: y (x if not stepped); DAdam forms: x
     }
     if constexpr (FUSED) {
       if ((a.active >> j) & 1ull) {
@@ -679,19 +710,29 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
         store_f32<V>(a.v + e, cnt, vv);
       }
     }
-    if (a.use_u) {
-      decode_raw<GASLOC_F32, V>(b.u[r], uv);
+    if constexpr (kEq) {
+      float uv[V];
+      if (a.use_u) {
+        decode_raw<GASLOC_F32, V>(b.pu[r], uv);
+      } else {
+#pragma unroll
+        for (int c = 0; c < V; ++c) uv[c] = 0.0f;
+      }
+#pragma unroll
+      for (int c = 0; c < V; ++c) out[c] = outer_step(xv[c], xv[c] - yv[c], uv[c], a.mu, a.eta, a.nesterov);
+      if (a.use_u) store_f32<V>(a.u + e, cnt, uv);
     } else {
 #pragma unroll
-      for (int c = 0; c < V; ++c) uv[c] = 0.0f;
+      for (int c = 0; c < V; ++c) out[c] = yv[c];
     }
-    float* out = mine + slot * slot_stride;
-#pragma unroll
-    for (int c = 0; c < V; ++c) out[c] = outer_step(xv[c], xv[c] - yv[c], uv[c], a.mu, a.eta, a.nesterov);
-    if (a.use_u) store_f32<V>(a.u + e, cnt, uv);
   }
 
-  // the rows: sum_k W_rk z_k in CSR order (+ gamma (z_r - zp_r)), zp_r = z_r
+  // the rows, each summing its CSR entries in order (four entries' LDS reads
+  // in flight at a time):
+  //   EQ:          x_r = sum_k W_rk z_k (+ gamma (z_r - zp_r)), zp_r = z_r
+  //   ALG1:        d = sum_k W_rk (x_r - y_k), outer step from x_r
+  //   DAdam:       x_r = sum_k W_rk x_k + (y_r - x_r)
+  //   Local-DAdam: d = sum_k W_rk (x_r - x_k), outer step from y_r
   const int rows_at = at + 2 + 2 * npre;
   int pos = rows_at + nrows;
 #pragma unroll
@@ -699,12 +740,25 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
     if (rr >= nrows) break;
     const int row = ops[rows_at + rr];
     const int nent = ops[pos];
-    const int own = ops[pos + 1];
     const int64_t er = static_cast<int64_t>(row) * a.ld + p;
+    float own[V];
+    {
+      const float* zo = mine + ops[pos + 1] * slot_stride;
+#pragma unroll
+      for (int c = 0; c < V; ++c) own[c] = zo[c];
+    }
+    // xi: the value the differences are taken from (ALG1, Local-DAdam)
+    float xi[V];
+    if constexpr (kAlg1) {
+      decode_raw<DT, V>(b.ra[rr], xi);
+    } else {
+#pragma unroll
+      for (int c = 0; c < V; ++c) xi[c] = own[c];
+    }
+    constexpr bool kDiff = kAlg1 || FORM == GASLOC_FORM_LOCAL_DADAM;
     float acc[V];
 #pragma unroll
     for (int c = 0; c < V; ++c) acc[c] = 0.0f;
-    // four entries' LDS reads in flight at a time, summed in CSR order
     for (int k0 = 0; k0 < nent; k0 += 4) {
       float zk[4][V], wk[4];
 #pragma unroll
@@ -719,23 +773,51 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
       for (int t = 0; t < 4; ++t) {
         if (k0 + t >= nent) break;
 #pragma unroll
-        for (int c = 0; c < V; ++c) acc[c] = acc[c] + wk[t] * zk[t][c];
+        for (int c = 0; c < V; ++c) acc[c] = acc[c] + wk[t] * (kDiff ? xi[c] - zk[t][c] : zk[t][c]);
       }
     }
     pos += 2 + 2 * nent;
-    const float* zo = mine + own * slot_stride;
-    float zcur[V];
+    float res[V];
+    if constexpr (kEq) {
+      if (a.apply_gamma) {
+        float zpv[V];
+        decode_raw<GASLOC_F32, V>(b.rf[rr], zpv);
 #pragma unroll
-    for (int c = 0; c < V; ++c) zcur[c] = zo[c];
-    if (a.apply_gamma) {
-      float zpv[V];
-      decode_raw<GASLOC_F32, V>(b.zp[rr], zpv);
+        for (int c = 0; c < V; ++c) acc[c] = acc[c] + a.gamma * (own[c] - zpv[c]);
+      }
+      if (a.store_zp) store_f32<V>(a.zp + er, cnt, own);
 #pragma unroll
-      for (int c = 0; c < V; ++c) acc[c] = acc[c] + a.gamma * (zcur[c] - zpv[c]);
+      for (int c = 0; c < V; ++c) res[c] = acc[c];
+    } else {
+      // DAdam forms: y_r, or x_r itself for a worker without local steps
+      float base[V];
+      if constexpr (kAlg1) {
+#pragma unroll
+        for (int c = 0; c < V; ++c) base[c] = xi[c];
+      } else if ((a.stepped >> row) & 1ull) {
+        decode_raw<DT, V>(b.ra[rr], base);
+      } else {
+#pragma unroll
+        for (int c = 0; c < V; ++c) base[c] = own[c];
+      }
+      if constexpr (FORM == GASLOC_FORM_DADAM) {
+#pragma unroll
+        for (int c = 0; c < V; ++c) res[c] = acc[c] + (base[c] - own[c]);
+      } else {
+        float uv[V];
+        if (a.use_u) {
+          decode_raw<GASLOC_F32, V>(b.rf[rr], uv);
+        } else {
+#pragma unroll
+          for (int c = 0; c < V; ++c) uv[c] = 0.0f;
+        }
+#pragma unroll
+        for (int c = 0; c < V; ++c) res[c] = outer_step(base[c], acc[c], uv[c], a.mu, a.eta, a.nesterov);
+        if (a.use_u) store_f32<V>(a.u + er, cnt, uv);
+      }
     }
-    if (a.store_zp) store_f32<V>(a.zp + er, cnt, zcur);
     float kept[V];
-    store_params<DT, V>(a.x, er, cnt, acc, kept);
+    store_params<DT, V>(a.x, er, cnt, res, kept);
 #pragma unroll
     for (int c = 0; c < V; ++c) {
       const double xd = static_cast<double>(kept[c]);
@@ -752,7 +834,7 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
   }
 }
 
-template <int DT, int V, int R, bool FUSED>
+template <int DT, int V, int R, bool FUSED, int FORM>
 __global__ __launch_bounds__(256) void k_gossip_planned(GossipArgs a) {
   extern __shared__ __align__(16) float zs[];  // [slots][nt][V]
   plan_word* ops = (plan_word*)(a.ops);  // address-space cast: read-only for the whole launch
@@ -782,14 +864,14 @@ __global__ __launch_bounds__(256) void k_gossip_planned(GossipArgs a) {
   int64_t it_issue = 0, it_use = 0;
   int st_issue = 0, st_use = 0;
   auto issue = [&](Staged<DT, V, R>& b) {
-    planned_issue<DT, V, R, false>(a, ops, st_issue, column(it_issue), V, b);
+    planned_issue<DT, V, R, FORM, false>(a, ops, st_issue, column(it_issue), V, b);
     if (++st_issue == steps) {
       st_issue = 0;
       ++it_issue;
     }
   };
   auto use = [&](const Staged<DT, V, R>& b) {
-    planned_consume<DT, V, R, FUSED, false>(a, ops, st_use, column(it_use), V, b, mine, slot_stride, cs);
+    planned_consume<DT, V, R, FUSED, FORM, false>(a, ops, st_use, column(it_use), V, b, mine, slot_stride, cs);
     if (++st_use == steps) {
 #pragma unroll
       for (int c = 0; c < V; ++c) ce += cs.q[c] - cs.s[c] * cs.s[c] * inv_n;
@@ -812,8 +894,8 @@ __global__ __launch_bounds__(256) void k_gossip_planned(GossipArgs a) {
     const int64_t left = a.P - col;
     const int cnt = left >= V ? V : (left > 0 ? static_cast<int>(left) : 0);
     for (int st = 0; st < steps; ++st) {
-      planned_issue<DT, V, R, true>(a, ops, st, col, cnt, A);
-      planned_consume<DT, V, R, FUSED, true>(a, ops, st, col, cnt, A, mine, slot_stride, cs);
+      planned_issue<DT, V, R, FORM, true>(a, ops, st, col, cnt, A);
+      planned_consume<DT, V, R, FUSED, FORM, true>(a, ops, st, col, cnt, A, mine, slot_stride, cs);
     }
 #pragma unroll
     for (int c = 0; c < V; ++c)
@@ -948,27 +1030,42 @@ size_t planned_lds_bytes(int slots, const LaunchShape& s) {
   return static_cast<size_t>(slots) * s.threads * s.vec * sizeof(float);
 }
 
-template <int DT, int V, bool FUSED>
+template <int DT, int V, bool FUSED, int FORM>
 hipError_t launch_planned_typed(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
-  hipLaunchKernelGGL((k_gossip_planned<DT, V, kPlanBatch, FUSED>), dim3(s.blocks), dim3(s.threads),
+  hipLaunchKernelGGL((k_gossip_planned<DT, V, kPlanBatch, FUSED, FORM>), dim3(s.blocks), dim3(s.threads),
                      planned_lds_bytes(a.slots, s), stream, a);
   return hipGetLastError();
 }
 
-template <int DT, bool FUSED>
+template <int DT, bool FUSED, int FORM>
 hipError_t launch_planned_vec(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
-  if (s.vec == 4) return launch_planned_typed<DT, 4, FUSED>(a, s, stream);
-  if (s.vec == 2) return launch_planned_typed<DT, 2, FUSED>(a, s, stream);
-  return launch_planned_typed<DT, 1, FUSED>(a, s, stream);
+  if (s.vec == 4) return launch_planned_typed<DT, 4, FUSED, FORM>(a, s, stream);
+  if (s.vec == 2) return launch_planned_typed<DT, 2, FUSED, FORM>(a, s, stream);
+  return launch_planned_typed<DT, 1, FUSED, FORM>(a, s, stream);
 }
 
-hipError_t launch_gossip_planned(const GossipArgs& a, int dtype, bool fused, const LaunchShape& s,
+// As for the phase kernel, the fused last step exists for EQ and ALG1.
+template <int DT>
+hipError_t launch_planned_dtype(const GossipArgs& a, bool fused, int form, const LaunchShape& s,
+                                hipStream_t stream) {
+  switch (form) {
+    case GASLOC_FORM_ALG1:
+      return fused ? launch_planned_vec<DT, true, GASLOC_FORM_ALG1>(a, s, stream)
+                   : launch_planned_vec<DT, false, GASLOC_FORM_ALG1>(a, s, stream);
+    case GASLOC_FORM_DADAM:
+      return launch_planned_vec<DT, false, GASLOC_FORM_DADAM>(a, s, stream);
+    case GASLOC_FORM_LOCAL_DADAM:
+      return launch_planned_vec<DT, false, GASLOC_FORM_LOCAL_DADAM>(a, s, stream);
+    default:
+      return fused ? launch_planned_vec<DT, true, GASLOC_FORM_EQ>(a, s, stream)
+                   : launch_planned_vec<DT, false, GASLOC_FORM_EQ>(a, s, stream);
+  }
+}
+
+hipError_t launch_gossip_planned(const GossipArgs& a, int dtype, bool fused, int form, const LaunchShape& s,
                                  hipStream_t stream) {
-  if (dtype == GASLOC_BF16)
-    return fused ? launch_planned_vec<GASLOC_BF16, true>(a, s, stream)
-                 : launch_planned_vec<GASLOC_BF16, false>(a, s, stream);
-  return fused ? launch_planned_vec<GASLOC_F32, true>(a, s, stream)
-               : launch_planned_vec<GASLOC_F32, false>(a, s, stream);
+  if (dtype == GASLOC_BF16) return launch_planned_dtype<GASLOC_BF16>(a, fused, form, s, stream);
+  return launch_planned_dtype<GASLOC_F32>(a, fused, form, s, stream);
 }
 
 hipError_t launch_gossip_round(const GossipArgs& a, int dtype, bool fused, int form, const LaunchShape& s,

@@ -263,19 +263,20 @@ gasloc_status upload_plan(gasloc_ctx* c, const std::vector<int32_t>& ops) {
   return GASLOC_OK;
 }
 
-// Which EQ-form kernel runs a round: the phase kernel keeps every worker's z
-// in LDS; the planned kernel (plan.cpp) keeps only the live ones.  Measured
-// on MI355X: planned is 2.3x faster at n=64 (1-Peer) and 1.9x at n=32
-// (3-regular), where LDS limits the phase kernel; at n <= 16 the phase
-// kernel fits and keeps more loads in flight (fused round at n=16: 45.0 vs
-// 48.2 ms), and a dense W needs a slot per worker anyway.
+// Which kernel runs a round: the phase kernel keeps every worker's slot
+// value in LDS; the planned kernel (plan.cpp) keeps only the live ones.
+// Measured on MI355X (EQ form): planned is 2.3x faster at n=64 (1-Peer) and
+// 1.9x at n=32 (3-regular), where LDS limits the phase kernel; at n <= 16 the
+// phase kernel fits and keeps more loads in flight (fused round at n=16: 45.0
+// vs 48.2 ms), and a dense W needs a slot per worker anyway.
 // Override for tuning sweeps: GASLOC_GOSSIP_KERNEL=phase|planned.
-bool use_planned(const gasloc_ctx& c, int slots) {
+enum class KernelChoice { kPhase, kPlanned, kBySlots };
+KernelChoice kernel_choice(const gasloc_ctx& c) {
   if (const char* env = std::getenv("GASLOC_GOSSIP_KERNEL")) {
-    if (std::strcmp(env, "phase") == 0) return false;
-    if (std::strcmp(env, "planned") == 0) return true;
+    if (std::strcmp(env, "phase") == 0) return KernelChoice::kPhase;
+    if (std::strcmp(env, "planned") == 0) return KernelChoice::kPlanned;
   }
-  return c.n > 16 && slots < c.n;
+  return c.n > 16 ? KernelChoice::kBySlots : KernelChoice::kPhase;
 }
 
 gasloc_status reduce_cols(gasloc_ctx* c, int64_t p0, int64_t p1) {
@@ -375,12 +376,12 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
   DeviceGuard guard(c->device);
   bool planned = false;
   int slots = 0;
-  if (c->hp.round_form == GASLOC_FORM_EQ) {
-    // super-steps of as many new z values as the kernel batches loads for
+  const KernelChoice choice = kernel_choice(*c);
+  if (choice != KernelChoice::kPhase) {
     std::string err;
     if (!gasloc::plan_round(c->n, rp, col, val, &c->plan_ops, &slots, &err))
       return fail(c, GASLOC_EINVAL, err);
-    planned = use_planned(*c, slots);
+    planned = choice == KernelChoice::kPlanned || slots < c->n;
   }
   gasloc::LaunchShape shape;
   size_t lds = 0;
@@ -456,7 +457,8 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
   if (planned) {
     a.ops = reinterpret_cast<const int32_t*>(c->d_csr);
     a.slots = slots;
-    HIP_TRY(c, gasloc::launch_gossip_planned(a, c->hp.param_dtype, step != nullptr, shape, c->stream));
+    HIP_TRY(c, gasloc::launch_gossip_planned(a, c->hp.param_dtype, step != nullptr, c->hp.round_form, shape,
+                                             c->stream));
   } else {
     HIP_TRY(c, gasloc::launch_gossip_round(a, c->hp.param_dtype, step != nullptr, c->hp.round_form, shape,
                                            c->stream));
