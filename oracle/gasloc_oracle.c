@@ -695,6 +695,22 @@ double orc_consensus_error(int n, int64_t P, int64_t ld, int dtype, const void *
   return total;
 }
 
+/* Squared norm of the round's pseudo-gradients, sum_i ||x_i - y_i||^2 (the
+ * outer-loop difference of Eq. 1 between the round anchor x_{t,0} and the
+ * live local iterate x_{t,H}; y = x for a worker without local steps).  The
+ * difference is taken in the working precision, as the round takes it; its
+ * square and the sums are fp64. */
+double orc_pseudo_gradient_sq(int n, int64_t P, int64_t ld, int dtype, const void *x, const void *y) {
+  double total = 0.0;
+  for (int i = 0; i < n; ++i)
+    for (int64_t p = 0; p < P; ++p) {
+      int64_t e = (int64_t)i * ld + p;
+      REAL d = load_param(x, dtype, e) - load_param(y, dtype, e);
+      total += (double)d * (double)d;
+    }
+  return total;
+}
+
 /* Network average xbar_p = (1/n) sum_i x_ip (Algorithm 1 output), summed in
  * fp64 in replica order, divided in fp64, rounded to the parameter storage. */
 void orc_replica_mean(int n, int64_t P, int64_t ld, int dtype, const void *x, void *out) {

@@ -88,6 +88,8 @@ def _load(tag):
     lib.orc_lr_schedule.argtypes = [_d, _i64, _i64, _d, _d, _d]
     lib.orc_consensus_error.restype = _d
     lib.orc_consensus_error.argtypes = [ctypes.c_int, _i64, _i64, ctypes.c_int, _vp]
+    lib.orc_pseudo_gradient_sq.restype = _d
+    lib.orc_pseudo_gradient_sq.argtypes = [ctypes.c_int, _i64, _i64, ctypes.c_int, _vp, _vp]
     lib.orc_replica_mean.restype = None
     lib.orc_replica_mean.argtypes = [ctypes.c_int, _i64, _i64, ctypes.c_int, _vp, _vp]
     lib.orc_f32_to_bf16.restype = ctypes.c_uint16
@@ -254,6 +256,7 @@ class Oracle:
         self.z = np.zeros(shape, dtype=self.real)
         self.k = np.zeros(self.n, dtype=np.int64)
         self.rounds_done = 0
+        self.pg_last = 0.0  # pseudo_gradient_sq() of the state the last round consumed
 
     # hyperparameters as the library receives them: fp32 values for the fp32
     # oracle, the exact values for the fp64 one
@@ -298,6 +301,7 @@ class Oracle:
         col = np.ascontiguousarray(col, dtype=np.int32)
         val = np.ascontiguousarray(val, dtype=self.real)
         hp = self.hp
+        self.pg_last = self.pseudo_gradient_sq()
         common = (self.n, self.P, self.P, self.pcode, _ptr(self.x), _ptr(self.y))
         outer = (self._h(hp.outer_momentum), self._h(hp.outer_lr), int(bool(hp.nesterov)))
         csr = (_ptr(row_ptr), _ptr(col), _ptr(val))
@@ -322,6 +326,14 @@ class Oracle:
             return self.L.orc_consensus_error(self.n, self.P, self.P, self.pcode, _ptr(self.x))
         sub = np.ascontiguousarray(self.x[:, cols])
         return self.L.orc_consensus_error(self.n, sub.shape[1], sub.shape[1], self.pcode, _ptr(sub))
+
+    def pseudo_gradient_sq(self, cols=None):
+        """sum_i ||x_i - y_i||^2 of the current anchors and live iterates (Eq. 1's
+        pseudo-gradients), over all columns or the slice/index array `cols`."""
+        if cols is None:
+            return self.L.orc_pseudo_gradient_sq(self.n, self.P, self.P, self.pcode, _ptr(self.x), _ptr(self.y))
+        sx, sy = np.ascontiguousarray(self.x[:, cols]), np.ascontiguousarray(self.y[:, cols])
+        return self.L.orc_pseudo_gradient_sq(self.n, sx.shape[1], sx.shape[1], self.pcode, _ptr(sx), _ptr(sy))
 
     def replica_mean(self):
         out = np.zeros(self.P, dtype=self.pdt)
