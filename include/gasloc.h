@@ -18,8 +18,9 @@
  *   - "device" pointers are HIP device memory on the GPU that is current
  *     when gasloc_init runs; "host" pointers are ordinary CPU memory.
  *   - All device work is enqueued on the stream given to gasloc_init.  Only
- *     gasloc_consensus_error, gasloc_consensus_error_cols and gasloc_destroy
- *     wait for the stream; kernel faults surface at the next blocking call.
+ *     gasloc_consensus_error, gasloc_consensus_error_cols,
+ *     gasloc_pseudo_gradient_sq and gasloc_destroy wait for the stream;
+ *     kernel faults surface at the next blocking call.
  *   - A context is not thread-safe; distinct contexts are independent.
  *   - After a device error every call on the context returns GASLOC_ESTATE.
  */
@@ -206,7 +207,15 @@ gasloc_status gasloc_local_step_gossip_round(gasloc_ctx *ctx, const float *grads
  * current, otherwise reduces x afresh.  Blocks until the stream reaches it. */
 gasloc_status gasloc_consensus_error(gasloc_ctx *ctx, double *out);
 
-/* The same sum restricted to columns [p_begin, p_end) (0 <= p_begin <=
+/* sum_i ||x_i - y_i||^2 over the pseudo-gradients the last gossip round
+ * consumed (Eq. 1: g_t^i = x_{t,H} - x_{t,0}; y_i = x_i for a worker
+ * without local steps; with the fused call, y_i is the iterate after the
+ * fused step).  Differences in fp32, squares and sums in fp64, reduced inside
+ * the round kernel at no extra HBM traffic.  0 before the first round.
+ * Blocks until the stream reaches it. */
+gasloc_status gasloc_pseudo_gradient_sq(gasloc_ctx *ctx, double *out);
+
+/* The consensus error restricted to columns [p_begin, p_end) (0 <= p_begin <=
  * p_end <= P): one GPU's share when columns are split across GPUs.  Always
  * reduces x afresh.  Blocks. */
 gasloc_status gasloc_consensus_error_cols(gasloc_ctx *ctx, int64_t p_begin, int64_t p_end,

@@ -54,7 +54,8 @@ struct AdamArgs {
 };
 
 // One gossip round; the consensus-error partial of every workgroup goes to
-// partials[blockIdx.x].
+// partials[blockIdx.x], its partial sum of squared pseudo-gradients to
+// pg_partials[blockIdx.x].
 struct GossipArgs {
   void* x;
   const void* y;
@@ -64,6 +65,7 @@ struct GossipArgs {
   const int32_t* col;
   const float* val;
   double* partials;
+  double* pg_partials;
   int64_t ld, P;
   int32_t n, nnz;
   float mu, eta, gamma;
@@ -115,6 +117,6 @@ hipError_t launch_replica_mean(const void* x, int dtype, int64_t ld, int n, int6
 // Dynamic LDS bytes one workgroup of the gossip kernel needs (z slots of
 // every thread plus the staged CSR); the kernel also uses kStaticLds bytes.
 size_t gossip_lds_bytes(int n, int nnz, const LaunchShape& shape);
-constexpr size_t kStaticLds = 1024 / 64 * sizeof(double);
+constexpr size_t kStaticLds = 2 * 1024 / 64 * sizeof(double);
 
 }  // namespace gasloc

@@ -197,6 +197,29 @@ __device__ __forceinline__ double block_sum(double v) {
   return total;
 }
 
+// Sums of `a` and `b` over the workgroup, valid in thread 0 (the round
+// kernels' consensus-error and pseudo-gradient partials).
+__device__ __forceinline__ void block_sum2(double a, double b, double& ta, double& tb) {
+  __shared__ double wave_part2[2][1024 / kWave];
+  a = wave_sum(a);
+  b = wave_sum(b);
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  if (lane == 0) {
+    wave_part2[0][wave] = a;
+    wave_part2[1][wave] = b;
+  }
+  __syncthreads();
+  ta = 0.0;
+  tb = 0.0;
+  if (threadIdx.x == 0) {
+    const int waves = (blockDim.x + kWave - 1) / kWave;
+    for (int w = 0; w < waves; ++w) {
+      ta += wave_part2[0][w];
+      tb += wave_part2[1][w];
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // a1: local AdamW step
 // ---------------------------------------------------------------------------
@@ -297,7 +320,7 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
   const double inv_n = 1.0 / static_cast<double>(n);
   const int64_t groups = (a.P + V - 1) / V;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * nt;
-  double ce = 0.0;
+  double ce = 0.0, pg = 0.0;  // consensus error, squared pseudo-gradients
   for (int64_t gi = static_cast<int64_t>(blockIdx.x) * nt + tid; gi < groups; gi += stride) {
     const int64_t p = gi * V;
     const int cnt = static_cast<int>(a.P - p < V ? a.P - p : V);
@@ -363,6 +386,11 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
           for (int c = 0; c < V; ++c) out[c] = outer_step(xv[r][c], xv[r][c] - yv[r][c], uv[r][c], a.mu,
                                                           a.eta, a.nesterov);
           if (a.use_u) store_f32<V>(a.u + e, cnt, uv[r]);
+#pragma unroll
+          for (int c = 0; c < V; ++c) {
+            const double d = static_cast<double>(xv[r][c] - yv[r][c]);
+            if (c < cnt) pg += d * d;
+          }
         } else if constexpr (kAlg1) {
 #pragma unroll
           for (int c = 0; c < V; ++c) out[c] = yv[r][c];
@@ -464,6 +492,15 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
             res[c] = outer_step(kAlg1 ? xi[c] : b0[r][c], d[c], b1v[r][c], a.mu, a.eta, a.nesterov);
           if (a.use_u) store_f32<V>(a.u + e, cnt, b1v[r]);
         }
+        if constexpr (!kEq) {
+          // pseudo-gradient x_i - y_i: ALG1 holds x_i in b0 and y_i in the
+          // slot, the DAdam forms the other way round
+#pragma unroll
+          for (int c = 0; c < V; ++c) {
+            const double d = static_cast<double>(kAlg1 ? b0[r][c] - own[c] : own[c] - b0[r][c]);
+            if (c < cnt) pg += d * d;
+          }
+        }
         float kept[V];
         store_params<DT, V>(a.x, e, cnt, res, kept);
 #pragma unroll
@@ -486,8 +523,12 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
     for (int c = 0; c < V; ++c)
       if (c < cnt) ce += q[c] - s[c] * s[c] * inv_n;
   }
-  const double total = block_sum(ce);
-  if (tid == 0) a.partials[blockIdx.x] = total;
+  double total_ce, total_pg;
+  block_sum2(ce, pg, total_ce, total_pg);
+  if (tid == 0) {
+    a.partials[blockIdx.x] = total_ce;
+    a.pg_partials[blockIdx.x] = total_pg;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -641,11 +682,13 @@ __device__ __forceinline__ void planned_issue(const GossipArgs& a, plan_word* op
 }
 
 // Running consensus-error sums of one column group (shifted by its first
-// stored row, as in k_gossip_round); `fresh` until that row is stored.
+// stored row, as in k_gossip_round); `fresh` until that row is stored.  pg:
+// this thread's running sum of squared pseudo-gradients x_i - y_i.
 template <int V>
 struct CeSums {
   double shift[V], s[V], q[V];
   bool fresh;
+  double pg;
 };
 
 template <int DT, int V, int R, bool FUSED, int FORM, bool TAIL>
@@ -721,6 +764,11 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
 #pragma unroll
       for (int c = 0; c < V; ++c) out[c] = outer_step(xv[c], xv[c] - yv[c], uv[c], a.mu, a.eta, a.nesterov);
       if (a.use_u) store_f32<V>(a.u + e, cnt, uv);
+#pragma unroll
+      for (int c = 0; c < V; ++c) {
+        const double d = static_cast<double>(xv[c] - yv[c]);
+        if (c < cnt) cs.pg += d * d;
+      }
     } else {
 #pragma unroll
       for (int c = 0; c < V; ++c) out[c] = yv[c];
@@ -789,7 +837,8 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
 #pragma unroll
       for (int c = 0; c < V; ++c) res[c] = acc[c];
     } else {
-      // DAdam forms: y_r, or x_r itself for a worker without local steps
+      // ALG1: x_r; DAdam forms: y_r, or x_r itself for a worker without local
+      // steps
       float base[V];
       if constexpr (kAlg1) {
 #pragma unroll
@@ -799,6 +848,13 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
       } else {
 #pragma unroll
         for (int c = 0; c < V; ++c) base[c] = own[c];
+      }
+      // pseudo-gradient x_r - y_r: ALG1 holds y_r in the slot, the DAdam
+      // forms hold x_r there
+#pragma unroll
+      for (int c = 0; c < V; ++c) {
+        const double d = static_cast<double>(kAlg1 ? base[c] - own[c] : own[c] - base[c]);
+        if (c < cnt) cs.pg += d * d;
       }
       if constexpr (FORM == GASLOC_FORM_DADAM) {
 #pragma unroll
@@ -860,6 +916,7 @@ __global__ __launch_bounds__(256) void k_gossip_planned(GossipArgs a) {
 
   Staged<DT, V, R> A, B;
   CeSums<V> cs;
+  cs.pg = 0.0;
   double ce = 0.0;
   int64_t it_issue = 0, it_use = 0;
   int st_issue = 0, st_use = 0;
@@ -901,8 +958,12 @@ __global__ __launch_bounds__(256) void k_gossip_planned(GossipArgs a) {
     for (int c = 0; c < V; ++c)
       if (c < cnt) ce += cs.q[c] - cs.s[c] * cs.s[c] * inv_n;
   }
-  const double block_total = block_sum(ce);
-  if (tid == 0) a.partials[blockIdx.x] = block_total;
+  double total_ce, total_pg;
+  block_sum2(ce, cs.pg, total_ce, total_pg);
+  if (tid == 0) {
+    a.partials[blockIdx.x] = total_ce;
+    a.pg_partials[blockIdx.x] = total_pg;
+  }
 }
 
 // ---------------------------------------------------------------------------

@@ -77,10 +77,10 @@ struct gasloc_ctx {
   hipEvent_t stage_done[kStageSlots] = {};
   bool stage_used[kStageSlots] = {};
   int stage_next = 0;
-  double* d_partials = nullptr;
+  double* d_partials = nullptr;  // [2 * partial_cap]: consensus error, then pseudo-gradient partials
   int partial_cap = 0;
-  double* d_ce = nullptr;
-  double* h_ce = nullptr;
+  double* d_ce = nullptr;  // [2]: consensus error, squared pseudo-gradients of the last round
+  double* h_ce = nullptr;  // [2] pinned
 
   int adam_blocks_total = 0;
   int reduce_blocks = 0;
@@ -454,6 +454,7 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
     std::memcpy(a.c2, step->c2, sizeof a.c2);
   }
   a.partials = c->d_partials;
+  a.pg_partials = c->d_partials + c->partial_cap;
   if (planned) {
     a.ops = reinterpret_cast<const int32_t*>(c->d_csr);
     a.slots = slots;
@@ -464,6 +465,7 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
                                            c->stream));
   }
   HIP_TRY(c, gasloc::launch_finalize(c->d_partials, shape.blocks, c->d_ce, c->stream));
+  HIP_TRY(c, gasloc::launch_finalize(a.pg_partials, shape.blocks, c->d_ce + 1, c->stream));
   if (step) {
     for (int i = 0; i < c->n; ++i)
       if ((step->active >> i) & 1ull) c->k[static_cast<size_t>(i)] += 1;
@@ -571,10 +573,10 @@ gasloc_status gasloc_init(int32_t n, int64_t P, const gasloc_topology* topology,
   c->partial_cap = kMaxGridBlocks;
 
   if ((e = hipMalloc(&c->d_csr, stage_bytes(n))) != hipSuccess) return init_fail(e, "hipMalloc csr");
-  if ((e = hipMalloc(&c->d_partials, sizeof(double) * c->partial_cap)) != hipSuccess)
+  if ((e = hipMalloc(&c->d_partials, 2 * sizeof(double) * c->partial_cap)) != hipSuccess)
     return init_fail(e, "hipMalloc partials");
-  if ((e = hipMalloc(&c->d_ce, sizeof(double))) != hipSuccess) return init_fail(e, "hipMalloc ce");
-  if ((e = hipHostMalloc(&c->h_ce, sizeof(double), hipHostMallocDefault)) != hipSuccess)
+  if ((e = hipMalloc(&c->d_ce, 2 * sizeof(double))) != hipSuccess) return init_fail(e, "hipMalloc ce");
+  if ((e = hipHostMalloc(&c->h_ce, 2 * sizeof(double), hipHostMallocDefault)) != hipSuccess)
     return init_fail(e, "hipHostMalloc ce");
   for (int i = 0; i < kStageSlots; ++i) {
     if ((e = hipHostMalloc(&c->h_stage[i], stage_bytes(n), hipHostMallocDefault)) != hipSuccess)
@@ -583,6 +585,8 @@ gasloc_status gasloc_init(int32_t n, int64_t P, const gasloc_topology* topology,
       return init_fail(e, "hipEventCreate");
   }
 
+  if ((e = hipMemsetAsync(c->d_ce, 0, 2 * sizeof(double), c->stream)) != hipSuccess)
+    return init_fail(e, "hipMemsetAsync");
   // zero the optimizer state of every worker: m, v, u, zp
   const size_t state_bytes = sizeof(float) * static_cast<size_t>(n) * static_cast<size_t>(b.ld);
   for (float* p : {b.m, b.v, b.u, b.zp}) {
@@ -673,6 +677,16 @@ gasloc_status gasloc_consensus_error(gasloc_ctx* c, double* out) {
     c->ce_current = true;
   }
   return read_ce(c, out);
+}
+
+gasloc_status gasloc_pseudo_gradient_sq(gasloc_ctx* c, double* out) {
+  if (!c || !out) return fail(c, GASLOC_EINVAL, "NULL argument");
+  if (c->failed) return fail(c, GASLOC_ESTATE, "context unusable after a device error: " + c->err);
+  DeviceGuard guard(c->device);
+  HIP_TRY(c, hipMemcpyAsync(c->h_ce + 1, c->d_ce + 1, sizeof(double), hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  *out = c->h_ce[1];
+  return GASLOC_OK;
 }
 
 gasloc_status gasloc_consensus_error_cols(gasloc_ctx* c, int64_t p_begin, int64_t p_end, double* out) {

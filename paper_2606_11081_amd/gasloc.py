@@ -69,6 +69,7 @@ _SIGNATURES = {
     "gasloc_local_step_gossip_round": (ctypes.c_int, [_vp, _vp, _i64, _vp, ctypes.c_float,
                                                       ctypes.POINTER(gasloc_csr), _u64]),
     "gasloc_consensus_error": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_double)]),
+    "gasloc_pseudo_gradient_sq": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_double)]),
     "gasloc_consensus_error_cols": (ctypes.c_int, [_vp, _i64, _i64, ctypes.POINTER(ctypes.c_double)]),
     "gasloc_replica_mean": (ctypes.c_int, [_vp, _vp]),
     "gasloc_topology_csr": (ctypes.c_int, [_vp, _u64, _vp, _vp, _vp, _i32, ctypes.POINTER(_i32)]),
@@ -204,6 +205,13 @@ def gasloc_local_step_gossip_round(ctx, grads, grad_ld, active=None, lr=0.0, W=N
 def gasloc_consensus_error(ctx):
     out = ctypes.c_double()
     _check(library().gasloc_consensus_error(ctx, ctypes.byref(out)), ctx)
+    return out.value
+
+
+def gasloc_pseudo_gradient_sq(ctx):
+    """sum_i ||x_i - y_i||^2 of the pseudo-gradients the last round consumed (fp64); blocks."""
+    out = ctypes.c_double()
+    _check(library().gasloc_pseudo_gradient_sq(ctx, ctypes.byref(out)), ctx)
     return out.value
 
 
@@ -358,6 +366,9 @@ class GASLoC:
 
     def consensus_error(self):
         return gasloc_consensus_error(self.ctx)
+
+    def pseudo_gradient_sq(self):
+        return gasloc_pseudo_gradient_sq(self.ctx)
 
     def consensus_error_cols(self, p_begin, p_end):
         return gasloc_consensus_error_cols(self.ctx, p_begin, p_end)

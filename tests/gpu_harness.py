@@ -115,6 +115,7 @@ class Pair:
                 rp, col, val = W
                 o.gossip_round(t, csr=(rp, col, val.astype(o.real)))
         self.step += 1
+        self.check_pg("fused round %d" % t)
 
     def gossip_round(self, t, W=None):
         self.gpu.gossip_round(t, W)
@@ -124,6 +125,14 @@ class Pair:
             else:
                 rp, col, val = W
                 o.gossip_round(t, csr=(rp, col, val.astype(o.real)))
+        self.check_pg("round %d" % t)
+
+    def check_pg(self, what):
+        """The round's fused pseudo-gradient statistic against the fp32 oracle's
+        (only when the oracle holds every column)."""
+        if not self.full or "f32" not in self.oracles:
+            return
+        reduction_close(self.gpu.pseudo_gradient_sq(), self.oracles["f32"].pg_last, "pseudo-gradient sq, " + what)
 
     def gather(self, name, rows=None):
         t = getattr(self.gpu, name)

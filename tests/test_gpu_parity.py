@@ -257,6 +257,7 @@ def test_nan_gradient_spreads_only_along_the_round_edges():
     assert np.array_equal(poisoned, W[:, bad] != 0), "NaN reaches exactly the workers that read worker %d" % bad
     assert not np.isnan(np.delete(x, 100, axis=1)).any(), "other columns stay finite"
     assert np.isnan(pair.gpu.consensus_error())
+    assert np.isnan(pair.gpu.pseudo_gradient_sq())
 
 
 def test_restricted_schedule_on_device():
@@ -379,7 +380,7 @@ def test_checkpoint_resume_is_bit_exact():
         full.gossip_round(t)
     torch.cuda.synchronize()
 
-    resumed = Pair(n, P, "two_peer", "f32", precisions=("f32",))
+    resumed = Pair(n, P, "two_peer", "f32", precisions=())  # compared with `full`, not an oracle
     torch.cuda.synchronize()
     for name, t_ in saved.items():
         getattr(resumed.gpu, name).copy_(t_)
@@ -392,6 +393,19 @@ def test_checkpoint_resume_is_bit_exact():
     for name in ("x", "m", "v", "u", "zp"):
         assert torch.equal(getattr(full.gpu, name)[:, :P], getattr(resumed.gpu, name)[:, :P]), name
     assert full.gpu.consensus_error() == resumed.gpu.consensus_error()
+    assert full.gpu.pseudo_gradient_sq() == resumed.gpu.pseudo_gradient_sq()
+
+
+@pytest.mark.parametrize("n,topology", [(8, "ring"), (40, "one_peer")])
+def test_pseudo_gradient_statistic_zero_cases(n, topology):
+    # 0 before any round, and for a round without local steps (y = x)
+    pair = Pair(n, 10_007, topology, "f32", gamma=0.1, precisions=("f32",))
+    assert pair.gpu.pseudo_gradient_sq() == 0.0
+    pair.local_step()
+    pair.gossip_round(0)  # checked against the oracle inside
+    assert pair.gpu.pseudo_gradient_sq() > 0.0
+    pair.gossip_round(1)
+    assert pair.gpu.pseudo_gradient_sq() == 0.0
 
 
 def test_consensus_error_columns_and_closed_form():
