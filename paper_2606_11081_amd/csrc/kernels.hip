@@ -1021,52 +1021,99 @@ __global__ __launch_bounds__(256) void k_replica_mean(const void* x, int64_t ld,
   }
 }
 
-template <int DT, int V, int R, bool FUSED, int FORM>
-hipError_t launch_gossip_typed(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
-  const size_t lds = gossip_lds_bytes(a.n, a.nnz, s);
-  hipLaunchKernelGGL((k_gossip_round<DT, V, R, FUSED, FORM>), dim3(s.blocks), dim3(s.threads), lds, stream,
-                     a);
-  return hipGetLastError();
+// Kernel selection, shared by the launchers and the occupancy queries: F is
+// called with the address of the instantiation that runs.
+template <int DT, int V, int R, bool FUSED, int FORM, typename F>
+hipError_t with_round_typed(F& f) {
+  return f(reinterpret_cast<const void*>(&k_gossip_round<DT, V, R, FUSED, FORM>));
 }
 
 // The fused kernel carries three more streams per worker, so it batches at
 // most 4 workers to stay within the register file.
-template <int DT, int V, bool FUSED, int FORM>
-hipError_t launch_gossip_batched(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
-  switch (s.batch) {
-    case 1: return launch_gossip_typed<DT, V, 1, FUSED, FORM>(a, s, stream);
-    case 2: return launch_gossip_typed<DT, V, 2, FUSED, FORM>(a, s, stream);
+template <int DT, int V, bool FUSED, int FORM, typename F>
+hipError_t with_round_batched(int batch, F& f) {
+  switch (batch) {
+    case 1: return with_round_typed<DT, V, 1, FUSED, FORM>(f);
+    case 2: return with_round_typed<DT, V, 2, FUSED, FORM>(f);
     case 8:
-      if constexpr (!FUSED) return launch_gossip_typed<DT, V, 8, FUSED, FORM>(a, s, stream);
+      if constexpr (!FUSED) return with_round_typed<DT, V, 8, FUSED, FORM>(f);
       [[fallthrough]];
-    default: return launch_gossip_typed<DT, V, 4, FUSED, FORM>(a, s, stream);
+    default: return with_round_typed<DT, V, 4, FUSED, FORM>(f);
   }
 }
 
-template <int DT, bool FUSED, int FORM>
-hipError_t launch_gossip_vec(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
-  if (s.vec == 4) return launch_gossip_batched<DT, 4, FUSED, FORM>(a, s, stream);
-  if (s.vec == 2) return launch_gossip_batched<DT, 2, FUSED, FORM>(a, s, stream);
-  return launch_gossip_batched<DT, 1, FUSED, FORM>(a, s, stream);
+template <int DT, bool FUSED, int FORM, typename F>
+hipError_t with_round_vec(const LaunchShape& s, F& f) {
+  if (s.vec == 4) return with_round_batched<DT, 4, FUSED, FORM>(s.batch, f);
+  if (s.vec == 2) return with_round_batched<DT, 2, FUSED, FORM>(s.batch, f);
+  return with_round_batched<DT, 1, FUSED, FORM>(s.batch, f);
 }
 
 // The fused last local step exists for the forms whose slots hold the new
 // local iterate or depend on it in phase 1 (EQ, ALG1).
-template <int DT>
-hipError_t launch_gossip_dtype(const GossipArgs& a, bool fused, int form, const LaunchShape& s,
-                               hipStream_t stream) {
+template <int DT, typename F>
+hipError_t with_round_dtype(bool fused, int form, const LaunchShape& s, F& f) {
   switch (form) {
     case GASLOC_FORM_ALG1:
-      return fused ? launch_gossip_vec<DT, true, GASLOC_FORM_ALG1>(a, s, stream)
-                   : launch_gossip_vec<DT, false, GASLOC_FORM_ALG1>(a, s, stream);
+      return fused ? with_round_vec<DT, true, GASLOC_FORM_ALG1>(s, f)
+                   : with_round_vec<DT, false, GASLOC_FORM_ALG1>(s, f);
     case GASLOC_FORM_DADAM:
-      return launch_gossip_vec<DT, false, GASLOC_FORM_DADAM>(a, s, stream);
+      return with_round_vec<DT, false, GASLOC_FORM_DADAM>(s, f);
     case GASLOC_FORM_LOCAL_DADAM:
-      return launch_gossip_vec<DT, false, GASLOC_FORM_LOCAL_DADAM>(a, s, stream);
+      return with_round_vec<DT, false, GASLOC_FORM_LOCAL_DADAM>(s, f);
     default:
-      return fused ? launch_gossip_vec<DT, true, GASLOC_FORM_EQ>(a, s, stream)
-                   : launch_gossip_vec<DT, false, GASLOC_FORM_EQ>(a, s, stream);
+      return fused ? with_round_vec<DT, true, GASLOC_FORM_EQ>(s, f) : with_round_vec<DT, false, GASLOC_FORM_EQ>(s, f);
   }
+}
+
+template <typename F>
+hipError_t with_round_kernel(int dtype, bool fused, int form, const LaunchShape& s, F& f) {
+  if (dtype == GASLOC_BF16) return with_round_dtype<GASLOC_BF16>(fused, form, s, f);
+  return with_round_dtype<GASLOC_F32>(fused, form, s, f);
+}
+
+template <int DT, int V, bool FUSED, int FORM, typename F>
+hipError_t with_planned_typed(F& f) {
+  return f(reinterpret_cast<const void*>(&k_gossip_planned<DT, V, kPlanBatch, FUSED, FORM>));
+}
+
+template <int DT, bool FUSED, int FORM, typename F>
+hipError_t with_planned_vec(const LaunchShape& s, F& f) {
+  if (s.vec == 4) return with_planned_typed<DT, 4, FUSED, FORM>(f);
+  if (s.vec == 2) return with_planned_typed<DT, 2, FUSED, FORM>(f);
+  return with_planned_typed<DT, 1, FUSED, FORM>(f);
+}
+
+// As for the phase kernel, the fused last step exists for EQ and ALG1.
+template <int DT, typename F>
+hipError_t with_planned_dtype(bool fused, int form, const LaunchShape& s, F& f) {
+  switch (form) {
+    case GASLOC_FORM_ALG1:
+      return fused ? with_planned_vec<DT, true, GASLOC_FORM_ALG1>(s, f)
+                   : with_planned_vec<DT, false, GASLOC_FORM_ALG1>(s, f);
+    case GASLOC_FORM_DADAM:
+      return with_planned_vec<DT, false, GASLOC_FORM_DADAM>(s, f);
+    case GASLOC_FORM_LOCAL_DADAM:
+      return with_planned_vec<DT, false, GASLOC_FORM_LOCAL_DADAM>(s, f);
+    default:
+      return fused ? with_planned_vec<DT, true, GASLOC_FORM_EQ>(s, f)
+                   : with_planned_vec<DT, false, GASLOC_FORM_EQ>(s, f);
+  }
+}
+
+template <typename F>
+hipError_t with_planned_kernel(int dtype, bool fused, int form, const LaunchShape& s, F& f) {
+  if (dtype == GASLOC_BF16) return with_planned_dtype<GASLOC_BF16>(fused, form, s, f);
+  return with_planned_dtype<GASLOC_F32>(fused, form, s, f);
+}
+
+// Launches `kernel` with the round arguments.
+hipError_t launch_round_args(const void* kernel, const GossipArgs& a, const LaunchShape& s, size_t lds,
+                             hipStream_t stream) {
+  GossipArgs arg = a;
+  void* args[] = {&arg};
+  const hipError_t e = hipLaunchKernel(kernel, dim3(s.blocks), dim3(s.threads), args, lds, stream);
+  return e != hipSuccess ? e : hipGetLastError();
 }
 
 }  // namespace
@@ -1091,48 +1138,26 @@ size_t planned_lds_bytes(int slots, const LaunchShape& s) {
   return static_cast<size_t>(slots) * s.threads * s.vec * sizeof(float);
 }
 
-template <int DT, int V, bool FUSED, int FORM>
-hipError_t launch_planned_typed(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
-  hipLaunchKernelGGL((k_gossip_planned<DT, V, kPlanBatch, FUSED, FORM>), dim3(s.blocks), dim3(s.threads),
-                     planned_lds_bytes(a.slots, s), stream, a);
-  return hipGetLastError();
-}
-
-template <int DT, bool FUSED, int FORM>
-hipError_t launch_planned_vec(const GossipArgs& a, const LaunchShape& s, hipStream_t stream) {
-  if (s.vec == 4) return launch_planned_typed<DT, 4, FUSED, FORM>(a, s, stream);
-  if (s.vec == 2) return launch_planned_typed<DT, 2, FUSED, FORM>(a, s, stream);
-  return launch_planned_typed<DT, 1, FUSED, FORM>(a, s, stream);
-}
-
-// As for the phase kernel, the fused last step exists for EQ and ALG1.
-template <int DT>
-hipError_t launch_planned_dtype(const GossipArgs& a, bool fused, int form, const LaunchShape& s,
-                                hipStream_t stream) {
-  switch (form) {
-    case GASLOC_FORM_ALG1:
-      return fused ? launch_planned_vec<DT, true, GASLOC_FORM_ALG1>(a, s, stream)
-                   : launch_planned_vec<DT, false, GASLOC_FORM_ALG1>(a, s, stream);
-    case GASLOC_FORM_DADAM:
-      return launch_planned_vec<DT, false, GASLOC_FORM_DADAM>(a, s, stream);
-    case GASLOC_FORM_LOCAL_DADAM:
-      return launch_planned_vec<DT, false, GASLOC_FORM_LOCAL_DADAM>(a, s, stream);
-    default:
-      return fused ? launch_planned_vec<DT, true, GASLOC_FORM_EQ>(a, s, stream)
-                   : launch_planned_vec<DT, false, GASLOC_FORM_EQ>(a, s, stream);
-  }
-}
-
 hipError_t launch_gossip_planned(const GossipArgs& a, int dtype, bool fused, int form, const LaunchShape& s,
                                  hipStream_t stream) {
-  if (dtype == GASLOC_BF16) return launch_planned_dtype<GASLOC_BF16>(a, fused, form, s, stream);
-  return launch_planned_dtype<GASLOC_F32>(a, fused, form, s, stream);
+  auto launch = [&](const void* k) { return launch_round_args(k, a, s, planned_lds_bytes(a.slots, s), stream); };
+  return with_planned_kernel(dtype, fused, form, s, launch);
 }
 
 hipError_t launch_gossip_round(const GossipArgs& a, int dtype, bool fused, int form, const LaunchShape& s,
                                hipStream_t stream) {
-  if (dtype == GASLOC_BF16) return launch_gossip_dtype<GASLOC_BF16>(a, fused, form, s, stream);
-  return launch_gossip_dtype<GASLOC_F32>(a, fused, form, s, stream);
+  auto launch = [&](const void* k) { return launch_round_args(k, a, s, gossip_lds_bytes(a.n, a.nnz, s), stream); };
+  return with_round_kernel(dtype, fused, form, s, launch);
+}
+
+int round_blocks_per_cu(int dtype, bool fused, int form, bool planned, const LaunchShape& s, size_t dyn_lds) {
+  int blocks = 0;
+  auto occupancy = [&](const void* k) {
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, k, s.threads, dyn_lds);
+  };
+  const hipError_t e =
+      planned ? with_planned_kernel(dtype, fused, form, s, occupancy) : with_round_kernel(dtype, fused, form, s, occupancy);
+  return e == hipSuccess ? blocks : 0;
 }
 
 hipError_t launch_consensus_error(const void* x, int dtype, int64_t ld, int n, int64_t p_begin,

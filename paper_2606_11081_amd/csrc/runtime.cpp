@@ -191,9 +191,15 @@ gasloc::LaunchShape pick_gossip_shape(const gasloc_ctx& c, int nnz) {
   return gasloc::LaunchShape{1, 64, 0, 8};
 }
 
-int gossip_blocks(const gasloc_ctx& c, const gasloc::LaunchShape& s, int nnz) {
-  const size_t lds = gasloc::gossip_lds_bytes(c.n, nnz, s) + gasloc::kStaticLds;
-  int per_cu = static_cast<int>(std::min<size_t>(c.lds_per_cu / std::max<size_t>(lds, 1), 8));
+// Grid of a round kernel: one workgroup per resident slot on every CU (the
+// kernels loop over their columns), no more than the columns need.  The
+// residency comes from the occupancy of the exact kernel that runs, so a
+// kernel limited by registers rather than LDS is not given a second, partial
+// wave of workgroups.
+int round_blocks(const gasloc_ctx& c, const gasloc::LaunchShape& s, bool fused, bool planned, size_t dyn_lds) {
+  int per_cu = gasloc::round_blocks_per_cu(c.hp.param_dtype, fused, c.hp.round_form, planned, s, dyn_lds);
+  if (per_cu <= 0)  // query failed: bound by LDS alone
+    per_cu = static_cast<int>(std::min<size_t>(c.lds_per_cu / (dyn_lds + gasloc::kStaticLds), 2048 / s.threads));
   per_cu = std::max(per_cu, 1);
   const int64_t groups = (c.P + s.vec - 1) / s.vec;
   const int64_t needed = (groups + s.threads - 1) / s.threads;
@@ -387,29 +393,27 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
   size_t lds = 0;
   if (planned) {
     // 4 columns per thread when the plan needs few slots (n=64 1-Peer: 10.7-
-    // 12.8 ms); with many slots 2 columns, so that four 256-thread workgroups
-    // fit a CU's LDS (n=32 3-regular bf16, 11-19 slots: 18.0-21.2 ms; 4
-    // columns in 128 threads measured the same); fewer columns, then fewer
-    // threads, while a workgroup would use more than a quarter of the LDS
+    // 12.8 ms); with many slots 2 columns (n=32 3-regular bf16, 11-19 slots:
+    // 18.0-21.2 ms; 4 columns in 128 threads measured the same).  While a
+    // workgroup would use more than a quarter of a CU's LDS, fewer threads
+    // first (2 columns in 128 threads keep 8-byte loads; 1 column was 25%
+    // slower), then fewer columns
     shape = gasloc::LaunchShape{slots <= 8 ? 4 : 2, 256, 0, gasloc::kPlanBatch};
-    if (gasloc::planned_lds_bytes(slots, shape) + gasloc::kStaticLds > c->lds_per_cu / 4) shape.vec = 2;
-    if (gasloc::planned_lds_bytes(slots, shape) + gasloc::kStaticLds > c->lds_per_cu / 4) shape.vec = 1;
-    while (shape.threads > 64 && gasloc::planned_lds_bytes(slots, shape) + gasloc::kStaticLds >
-                                     std::min(c->lds_per_cu / 2, c->lds_per_block_max))
-      shape.threads /= 2;
+    auto over = [&] { return gasloc::planned_lds_bytes(slots, shape) + gasloc::kStaticLds > c->lds_per_cu / 4; };
+    while (shape.threads > 64 && over()) shape.threads /= 2;
+    while (shape.vec > 1 && over()) shape.vec /= 2;
     apply_shape_override(&shape);
     lds = gasloc::planned_lds_bytes(slots, shape) + gasloc::kStaticLds;
-    const int per_cu = std::max(1, static_cast<int>(std::min<size_t>(c->lds_per_cu / lds, 8)));
-    const int64_t needed = ((c->P + shape.vec - 1) / shape.vec + shape.threads - 1) / shape.threads;
     if (shape.blocks == 0)
-      shape.blocks = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(needed, int64_t(c->cus) * per_cu)));
+      shape.blocks = round_blocks(*c, shape, step != nullptr, true, gasloc::planned_lds_bytes(slots, shape));
   } else {
     shape = pick_gossip_shape(*c, nnz);
     if (step) shape.batch = 4;
-    shape.blocks = gossip_blocks(*c, shape, nnz);
     apply_shape_override(&shape);
-    if (shape.blocks == 0) shape.blocks = gossip_blocks(*c, shape, nnz);
+    if (step && shape.batch == 8) shape.batch = 4;  // the fused kernel batches at most 4 workers
     lds = gasloc::gossip_lds_bytes(c->n, nnz, shape) + gasloc::kStaticLds;
+    if (shape.blocks == 0)
+      shape.blocks = round_blocks(*c, shape, step != nullptr, false, gasloc::gossip_lds_bytes(c->n, nnz, shape));
   }
   shape.blocks = std::min(shape.blocks, c->partial_cap);
   if (lds > c->lds_per_block_max) return fail(c, GASLOC_EINVAL, "gossip shape exceeds the device's LDS per workgroup");
