@@ -173,13 +173,40 @@ __device__ __forceinline__ float as_stored(float v) {
 }
 
 // ---------------------------------------------------------------------------
-// reductions: fixed-order wave shuffle, then the waves of the workgroup
+// reductions: fixed-order DPP scan inside the wave, then the waves of the
+// workgroup
 // ---------------------------------------------------------------------------
 
+// v from the lane `k` places lower in the same 16-lane row (DPP row_shr:k),
+// 0 for the first k lanes of each row.  A double moves as two 32-bit halves.
+template <int K>
+__device__ __forceinline__ double row_shr(double v) {
+  const uint64_t bits = static_cast<uint64_t>(__double_as_longlong(v));
+  const int lo = __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(bits)), 0x110 + K, 0xf, 0xf,
+                                             true);
+  const int hi = __builtin_amdgcn_update_dpp(0, static_cast<int>(static_cast<uint32_t>(bits >> 32)), 0x110 + K, 0xf,
+                                             0xf, true);
+  return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) |
+                                                     static_cast<uint32_t>(lo)));
+}
+
+__device__ __forceinline__ double read_lane(double v, int lane) {
+  const uint64_t bits = static_cast<uint64_t>(__double_as_longlong(v));
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(bits)), lane));
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(bits >> 32)), lane));
+  return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
+}
+
+// Sum over the wave (all 64 lanes active), the same in every lane: an
+// inclusive scan inside each 16-lane row with DPP row shifts (lane 15 of a
+// row then holds the row's sum), and the four row sums added in row order.
+// The order of additions is fixed, so the result is deterministic.
 __device__ __forceinline__ double wave_sum(double v) {
-#pragma unroll
-  for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_down(v, off, kWave);
-  return v;
+  v += row_shr<1>(v);
+  v += row_shr<2>(v);
+  v += row_shr<4>(v);
+  v += row_shr<8>(v);
+  return ((read_lane(v, 15) + read_lane(v, 31)) + read_lane(v, 47)) + read_lane(v, 63);
 }
 
 // Sum of `v` over the workgroup, valid in thread 0.
