@@ -293,8 +293,8 @@ __global__ __launch_bounds__(256) void k_local_adamw(AdamArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// a2-a5: pseudo-gradient, outer step, neighbour mix, consensus momentum and
-// the consensus-error partial, fused.  A thread owns V consecutive columns
+// a2-a5: pseudo-gradient, outer step, neighbour mix, consensus momentum, and
+// the consensus-error and squared-pseudo-gradient partials, fused.  A thread owns V consecutive columns
 // of *every* worker, so each element of x, y, u, zp is read and written
 // exactly once and the in-place updates cannot race.  Phase 1 puts one value
 // per worker in this thread's private LDS slots (no barrier is needed
@@ -559,12 +559,13 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// The EQ round with a host-planned visit order (plan.cpp).  Each super-step
-// computes the z of the workers its rows read first (at most R of them) into
-// free LDS slots, then emits up to kPlanRows rows.  LDS holds `slots` values
-// per column instead of n, so sparse graphs keep many more columns in flight
-// per CU.  Per element the arithmetic is exactly that of
-// k_gossip_round<..., GASLOC_FORM_EQ>.
+// A round of any form with a host-planned visit order (plan.cpp).  Each
+// super-step computes the slot values (z for EQ, the live local iterate for
+// ALG1, x for the DAdam forms) of the workers its rows read first (at most R
+// of them) into free LDS slots, then emits up to kPlanRows rows.  LDS holds
+// `slots` values per column instead of n, so sparse graphs keep many more
+// columns in flight per CU.  Per element the arithmetic is exactly that of
+// k_gossip_round<..., FORM>.
 //
 // The plan is the same for every column, so it is read through the scalar
 // cache (constant address space): worker and slot indices, counts and weights
