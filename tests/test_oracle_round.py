@@ -355,6 +355,29 @@ def test_consensus_error_definition():
     np.testing.assert_allclose(o.replica_mean(), 0.25)
 
 
+@pytest.mark.parametrize("precision,param_dtype", [("f64", "f32"), ("f32", "f32"), ("f32", "bf16")])
+def test_replica_mean_is_the_network_average(precision, param_dtype):
+    # Algorithm 1's output: the average of the n replicas, rounded once to the
+    # parameter storage (numpy's fp64 mean, then the storage rounding)
+    n, P = 7, 3000
+    rng = np.random.default_rng(12)
+    o = make_oracle(n, P, precision=precision, param_dtype=param_dtype)
+    x = rng.standard_normal((n, P)) * 0.3 + rng.standard_normal(P) * 2.0
+    if param_dtype == "bf16":
+        o.x[...] = oracle.f32_to_bf16_bits(x.astype(np.float32))
+        xs = oracle.bf16_bits_to_f32(o.x).astype(np.float64)
+        expect = oracle.f32_to_bf16_bits(np.mean(xs, axis=0).astype(np.float32))
+        assert np.array_equal(o.replica_mean(), expect)
+    else:
+        o.x[...] = x.astype(o.real)
+        expect = np.mean(o.x.astype(np.float64), axis=0).astype(o.real)
+        got = o.replica_mean()
+        if precision == "f64":
+            np.testing.assert_allclose(got, expect, rtol=1e-15, atol=1e-15)
+        else:
+            assert np.array_equal(got.view(np.uint32), expect.view(np.uint32))
+
+
 def _pure_gossip_oracle(n, P, csr, gamma, x):
     o = make_oracle(n, P, precision="f64", gamma=gamma)
     o.x[...] = x
