@@ -118,7 +118,7 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--cpu-columns", type=int, default=24_000_000)
+    ap.add_argument("--cpu-columns", type=int, default=30_000_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-gb", type=float, default=8.0, help="size of the copy probe (GB read)")
     ap.add_argument("--no-fuse", dest="fuse", action="store_false",
