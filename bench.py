@@ -108,15 +108,26 @@ def cpu_baseline(w, H_i, columns):
     dt = time.perf_counter() - t0
     return {"value": w.n * columns / dt, "unit": "replica-param updates/s", "cores": 1, "kind": "oracle",
             "sample": "%d of %d columns x %d workers, one round (%d local steps + gossip + CE), "
-                      "plain C oracle (fp32 build, -O2, single thread): %.2f s"
-                      % (columns, w.P, w.n, int(H_i.max()), dt)}
+                      "plain C oracle (fp32 build, -O2, single thread on %s, %d host threads visible): %.2f s"
+                      % (columns, w.P, w.n, int(H_i.max()), host_cpu(), os.cpu_count() or 0, dt)}
+
+
+def host_cpu():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown CPU"
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-columns", type=int, default=30_000_000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -127,7 +138,7 @@ def main():
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: every replica of the round lives on a single MI355X; "
-              "runs on %d GPUs are not part of this build" % max(args.gpus, 1), file=sys.stderr)
+              "multi-GPU runs (%d requested) are not supported" % max(args.gpus, 1), file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -187,9 +198,12 @@ def main():
     ev = {"adam": [], "round": []}
     ces = []
     torch.cuda.synchronize()
+    wall = []  # per round: each round ends with the blocking consensus-error readback
     t0 = time.perf_counter()
     for s in range(args.steps):
+        r0 = time.perf_counter()
         ces.append(one_round(args.warmup + s, ev))
+        wall.append((time.perf_counter() - r0) * 1e3)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_step = elapsed / args.steps * 1e3
@@ -212,7 +226,7 @@ def main():
 
     # the standalone gossip kernel (no fused step), timed after the rounds
     g_ms = []
-    for s in range(3):
+    for s in range(5):
         lib.local_step(grads, gi.LOCAL_LR)
         e = rec({"g": []}, "g")
         lib.gossip_round(args.warmup + args.steps + s)
@@ -254,6 +268,7 @@ def main():
         "unit": "replica-param updates/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_step, 3),
+        "round_ms_p10_p50_p90": [round(float(np.percentile(wall, q)), 3) for q in (10, 50, 90)],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": w.param_dtype, "data": "synthetic",
         "config": {"workload": w.name, "n": w.n, "P": w.P, "topology": w.topology,
