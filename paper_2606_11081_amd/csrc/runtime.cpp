@@ -196,11 +196,29 @@ gasloc::LaunchShape pick_gossip_shape(const gasloc_ctx& c, int nnz) {
 // residency comes from the occupancy of the exact kernel that runs, so a
 // kernel limited by registers rather than LDS is not given a second, partial
 // wave of workgroups.
+//
+// LDS is given to a workgroup in granules of 1/128 of the CU's LDS (1280 B
+// on MI355X).  The occupancy query counts LDS more finely and over-counts
+// LDS-bound residency: measured on the n=32 random 3-regular workload, 128-
+// and 64-thread workgroups whose LDS rounds up to one more granule ran a
+// partial second wave (30 ms instead of 20 ms) exactly in the rounds the
+// granule count predicts, so the LDS bound is applied here as well.
+int lds_blocks_per_cu(const gasloc_ctx& c, size_t dyn_lds) {
+  const size_t granule = std::max<size_t>(c.lds_per_cu / 128, 1);
+  const size_t held = (dyn_lds + gasloc::kStaticLds + granule - 1) / granule * granule;
+  return static_cast<int>(c.lds_per_cu / held);
+}
+
+// Workgroups of a round kernel resident on one CU at once (at least 1).
+int resident_blocks_per_cu(const gasloc_ctx& c, const gasloc::LaunchShape& s, bool fused, bool planned,
+                           size_t dyn_lds) {
+  const int by_lds = std::min(lds_blocks_per_cu(c, dyn_lds), 2048 / s.threads);
+  const int query = gasloc::round_blocks_per_cu(c.hp.param_dtype, fused, c.hp.round_form, planned, s, dyn_lds);
+  return std::max(1, query <= 0 ? by_lds : std::min(query, by_lds));  // a failed query leaves the LDS bound
+}
+
 int round_blocks(const gasloc_ctx& c, const gasloc::LaunchShape& s, bool fused, bool planned, size_t dyn_lds) {
-  int per_cu = gasloc::round_blocks_per_cu(c.hp.param_dtype, fused, c.hp.round_form, planned, s, dyn_lds);
-  if (per_cu <= 0)  // query failed: bound by LDS alone
-    per_cu = static_cast<int>(std::min<size_t>(c.lds_per_cu / (dyn_lds + gasloc::kStaticLds), 2048 / s.threads));
-  per_cu = std::max(per_cu, 1);
+  const int per_cu = resident_blocks_per_cu(c, s, fused, planned, dyn_lds);
   const int64_t groups = (c.P + s.vec - 1) / s.vec;
   const int64_t needed = (groups + s.threads - 1) / s.threads;
   return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(needed, int64_t(c.cus) * per_cu)));
@@ -393,15 +411,30 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
   size_t lds = 0;
   if (planned) {
     // 4 columns per thread when the plan needs few slots (n=64 1-Peer: 10.7-
-    // 12.8 ms); with many slots 2 columns (n=32 3-regular bf16, 11-19 slots:
-    // 18.0-21.2 ms; 4 columns in 128 threads measured the same).  While a
-    // workgroup would use more than a quarter of a CU's LDS, fewer threads
-    // first (2 columns in 128 threads keep 8-byte loads; 1 column was 25%
-    // slower), then fewer columns
+    // 12.8 ms), else 2 (1 column was 25% slower).  The workgroup size is the
+    // one that keeps the most waves resident per CU (LDS granules, registers;
+    // ties to the larger workgroup): on the n=32 random 3-regular workload,
+    // 256 threads for 14-15 slots (5 workgroups, 20 waves, 19.3-19.5 ms) and
+    // 128 threads for 16-19 slots (8-9 workgroups, 16-18 waves, 20.5 ms
+    // against 21.5-22.0 ms with 4 workgroups of 256).
     shape = gasloc::LaunchShape{slots <= 8 ? 4 : 2, 256, 0, gasloc::kPlanBatch};
-    auto over = [&] { return gasloc::planned_lds_bytes(slots, shape) + gasloc::kStaticLds > c->lds_per_cu / 4; };
-    while (shape.threads > 64 && over()) shape.threads /= 2;
-    while (shape.vec > 1 && over()) shape.vec /= 2;
+    {
+      int best_waves = -1;
+      gasloc::LaunchShape best = shape;
+      for (int vec = shape.vec; vec >= 1 && best_waves < 0; vec /= 2) {
+        for (int threads : {256, 128, 64}) {
+          gasloc::LaunchShape s{vec, threads, 0, gasloc::kPlanBatch};
+          const size_t dyn = gasloc::planned_lds_bytes(slots, s);
+          if (dyn + gasloc::kStaticLds > std::min(c->lds_per_cu / 2, c->lds_per_block_max)) continue;
+          const int waves = resident_blocks_per_cu(*c, s, step != nullptr, true, dyn) * (threads / 64);
+          if (waves > best_waves) {
+            best_waves = waves;
+            best = s;
+          }
+        }
+      }
+      shape = best;
+    }
     apply_shape_override(&shape);
     lds = gasloc::planned_lds_bytes(slots, shape) + gasloc::kStaticLds;
     if (shape.blocks == 0)
