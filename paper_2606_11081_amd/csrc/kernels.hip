@@ -39,6 +39,7 @@ __device__ __forceinline__ uint32_t f32_to_bf16(float f) {
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // Streaming data is touched once per kernel, so the vector accesses carry the
 // non-temporal hint (measured 2-4% faster on the n=16, P=350M round than
@@ -103,7 +104,13 @@ __device__ __forceinline__ void store_f32(float* p, int cnt, const float (&o)[V]
 template <int V>
 __device__ __forceinline__ void load_bf16(const uint16_t* p, int cnt, float (&o)[V]) {
   if (cnt == V) {
-    if constexpr (V == 4) {
+    if constexpr (V == 8) {
+      const u32x4 t = ld_stream(reinterpret_cast<const u32x4*>(p));
+      o[0] = bf16_to_f32(t.x & 0xffffu); o[1] = bf16_to_f32(t.x >> 16);
+      o[2] = bf16_to_f32(t.y & 0xffffu); o[3] = bf16_to_f32(t.y >> 16);
+      o[4] = bf16_to_f32(t.z & 0xffffu); o[5] = bf16_to_f32(t.z >> 16);
+      o[6] = bf16_to_f32(t.w & 0xffffu); o[7] = bf16_to_f32(t.w >> 16);
+    } else if constexpr (V == 4) {
       const u32x2 t = ld_stream(reinterpret_cast<const u32x2*>(p));
       o[0] = bf16_to_f32(t.x & 0xffffu); o[1] = bf16_to_f32(t.x >> 16);
       o[2] = bf16_to_f32(t.y & 0xffffu); o[3] = bf16_to_f32(t.y >> 16);
@@ -129,7 +136,10 @@ __device__ __forceinline__ void store_bf16(uint16_t* p, int cnt, const float (&o
     kept[c] = bf16_to_f32(h[c]);
   }
   if (cnt == V) {
-    if constexpr (V == 4) {
+    if constexpr (V == 8) {
+      st_stream(reinterpret_cast<u32x4*>(p), u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                                                   h[6] | (h[7] << 16)});
+    } else if constexpr (V == 4) {
       st_stream(reinterpret_cast<u32x2*>(p), u32x2{h[0] | (h[1] << 16), h[2] | (h[3] << 16)});
     } else if constexpr (V == 2) {
       st_stream(reinterpret_cast<uint32_t*>(p), h[0] | (h[1] << 16));
@@ -998,26 +1008,79 @@ __global__ __launch_bounds__(256) void k_gossip_planned(GossipArgs a) {
 // a5 standalone: consensus error of the stored x over columns [p_begin, p_end)
 // ---------------------------------------------------------------------------
 
+// Columns [lo, hi) of the V-column group at idx (the others read as 0): a
+// vector load when the whole group is in range.
+template <int DT, int V>
+__device__ __forceinline__ void load_cols(const void* base, int64_t idx, int lo, int hi, float (&o)[V]) {
+  if (lo == 0 && hi == V) {
+    load_params<DT, V>(base, idx, V, o);
+    return;
+  }
+#pragma unroll
+  for (int c = 0; c < V; ++c) {
+    if (c >= lo && c < hi) {
+      if constexpr (DT == GASLOC_BF16)
+        o[c] = bf16_to_f32(static_cast<const uint16_t*>(base)[idx + c]);
+      else
+        o[c] = static_cast<const float*>(base)[idx + c];
+    } else {
+      o[c] = 0.0f;
+    }
+  }
+}
+
+// A thread takes a group of columns of every worker (4 fp32 or 8 bf16, i.e.
+// 16 bytes; groups are aligned so every row's vector loads are, and the
+// groups at the ends of the range are masked), with the loads of 8 workers in
+// flight at a time.  Per column
+// the sums are those of the fused kernel: shifted by worker 0's value, fp64,
+// workers in order.
 template <int DT>
 __global__ __launch_bounds__(256) void k_consensus_error(const void* x, int64_t ld, int n,
                                                          int64_t p_begin, int64_t p_end,
                                                          double* partials) {
+  constexpr int V = DT == GASLOC_BF16 ? 8 : 4, R = 8;
   const double inv_n = 1.0 / static_cast<double>(n);
+  const int64_t base = p_begin - p_begin % V;
+  const int64_t groups = (p_end - base + V - 1) / V;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
   double ce = 0.0;
-  for (int64_t p = p_begin + static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; p < p_end;
-       p += stride) {
-    float v[1];
-    load_params<DT, 1>(x, p, 1, v);
-    const double shift = v[0];
-    double s = 0.0, q = 0.0;
-    for (int i = 1; i < n; ++i) {
-      load_params<DT, 1>(x, static_cast<int64_t>(i) * ld + p, 1, v);
-      const double d = static_cast<double>(v[0]) - shift;
-      s += d;
-      q += d * d;
+  for (int64_t gi = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; gi < groups; gi += stride) {
+    const int64_t p = base + gi * V;
+    const int lo = p < p_begin ? static_cast<int>(p_begin - p) : 0;
+    const int hi = p_end - p < V ? static_cast<int>(p_end - p) : V;
+    double shift[V], s[V], q[V];
+    {
+      float v[V];
+      load_cols<DT, V>(x, p, lo, hi, v);
+#pragma unroll
+      for (int c = 0; c < V; ++c) {
+        shift[c] = static_cast<double>(v[c]);
+        s[c] = 0.0;
+        q[c] = 0.0;
+      }
     }
-    ce += q - s * s * inv_n;
+    for (int i0 = 1; i0 < n; i0 += R) {
+      float v[R][V];
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (i0 + r >= n) break;
+        load_cols<DT, V>(x, static_cast<int64_t>(i0 + r) * ld + p, lo, hi, v[r]);
+      }
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (i0 + r >= n) break;
+#pragma unroll
+        for (int c = 0; c < V; ++c) {
+          const double d = static_cast<double>(v[r][c]) - shift[c];
+          s[c] += d;
+          q[c] += d * d;
+        }
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < V; ++c)
+      if (c >= lo && c < hi) ce += q[c] - s[c] * s[c] * inv_n;
   }
   const double total = block_sum(ce);
   if (threadIdx.x == 0) partials[blockIdx.x] = total;
@@ -1031,21 +1094,38 @@ __global__ __launch_bounds__(256) void k_finalize(const double* partials, int co
   if (threadIdx.x == 0) *out = total;
 }
 
-// a6: network average, fp64 sum in worker order, rounded to the param dtype
+// a6: network average, fp64 sum in worker order, rounded to the param dtype;
+// 16 bytes of columns per thread, the loads of 8 workers in flight at a time.
 template <int DT>
 __global__ __launch_bounds__(256) void k_replica_mean(const void* x, int64_t ld, int n, int64_t P,
                                                       void* out) {
+  constexpr int V = DT == GASLOC_BF16 ? 8 : 4, R = 8;
+  const int64_t groups = (P + V - 1) / V;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
-  for (int64_t p = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; p < P; p += stride) {
-    double s = 0.0;
-    for (int i = 0; i < n; ++i) {
-      float v[1];
-      load_params<DT, 1>(x, static_cast<int64_t>(i) * ld + p, 1, v);
-      s += static_cast<double>(v[0]);
+  for (int64_t gi = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; gi < groups; gi += stride) {
+    const int64_t p = gi * V;
+    const int cnt = static_cast<int>(P - p < V ? P - p : V);
+    double s[V];
+#pragma unroll
+    for (int c = 0; c < V; ++c) s[c] = 0.0;
+    for (int i0 = 0; i0 < n; i0 += R) {
+      float v[R][V];
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (i0 + r >= n) break;
+        load_params<DT, V>(x, static_cast<int64_t>(i0 + r) * ld + p, cnt, v[r]);
+      }
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (i0 + r >= n) break;
+#pragma unroll
+        for (int c = 0; c < V; ++c) s[c] += static_cast<double>(v[r][c]);
+      }
     }
-    const float mean[1] = {static_cast<float>(s / static_cast<double>(n))};
-    float kept[1];
-    store_params<DT, 1>(out, p, 1, mean, kept);
+    float mean[V], kept[V];
+#pragma unroll
+    for (int c = 0; c < V; ++c) mean[c] = static_cast<float>(s[c] / static_cast<double>(n));
+    store_params<DT, V>(out, p, cnt, mean, kept);
   }
 }
 
