@@ -1031,15 +1031,15 @@ __device__ __forceinline__ void load_cols(const void* base, int64_t idx, int lo,
 
 // A thread takes a group of columns of every worker (4 fp32 or 8 bf16, i.e.
 // 16 bytes; groups are aligned so every row's vector loads are, and the
-// groups at the ends of the range are masked), with the loads of 8 workers in
-// flight at a time.  Per column
+// groups at the ends of the range are masked), with the loads of 8 workers
+// (fp32) or 4 (bf16, twice the columns; 8 left it register-bound) in flight.  Per column
 // the sums are those of the fused kernel: shifted by worker 0's value, fp64,
 // workers in order.
 template <int DT>
 __global__ __launch_bounds__(256) void k_consensus_error(const void* x, int64_t ld, int n,
                                                          int64_t p_begin, int64_t p_end,
                                                          double* partials) {
-  constexpr int V = DT == GASLOC_BF16 ? 8 : 4, R = 8;
+  constexpr int V = DT == GASLOC_BF16 ? 8 : 4, R = DT == GASLOC_BF16 ? 4 : 8;
   const double inv_n = 1.0 / static_cast<double>(n);
   const int64_t base = p_begin - p_begin % V;
   const int64_t groups = (p_end - base + V - 1) / V;
