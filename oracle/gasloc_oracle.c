@@ -17,7 +17,11 @@
  *     gamma * [(x_t+eta g_t) - (x_{t-1}+eta g_{t-1})] (Eq. 2, momentum update);
  *   - consensus error ||pi x||^2 = sum_i ||x_i - xbar||^2 (section 3.1,
  *     Notation: pi is the projector onto the disagreement subspace);
+ *   - the squared pseudo-gradient norms sum_i ||x_i - y_i||^2 (Eq. 1);
  *   - network average (Algorithm 1 output);
+ *   - the round forms of Algorithm 1 and of App. C (DAdam, Local-DAdam), the
+ *     learning-rate schedule of App. B and skipped exchanges (section 3.2,
+ *     fault tolerance);
  *   - the communication graphs of section 3.2 and App. B.1 (random 1-Peer
  *     matching, random 2-Peer cycle), the static ring and complete graph
  *     of Tables 1-3, and the exponential graphs cited in section 3.2.
