@@ -28,6 +28,14 @@ def log(msg):
 def within(a, b, rel=REL, what=""):
     a = np.asarray(a, dtype=np.float64)
     b = np.asarray(b, dtype=np.float64)
+    # non-finite reference values must be reproduced exactly (the same
+    # infinity, or a NaN); the tolerance applies to the finite ones
+    nonfinite = ~np.isfinite(b)
+    if nonfinite.any():
+        an, bn = a[nonfinite], b[nonfinite]
+        ok = (an == bn) | (np.isnan(an) & np.isnan(bn))
+        assert ok.all(), "%s: %d non-finite reference values not reproduced" % (what, int((~ok).sum()))
+        a, b = a[~nonfinite], b[~nonfinite]
     rms = math.sqrt(float(np.mean(b * b))) if b.size else 0.0
     err = np.abs(a - b)
     bad = err > rel * np.abs(b) + rel * rms
