@@ -537,14 +537,15 @@ def test_full_size_sampled(name, sample, rounds):
     torch.cuda.empty_cache()
 
 
-def test_extreme_gradients_bit_exact():
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_extreme_gradients_bit_exact(dtype):
     # IEEE behaviour the op order relies on: subnormal squares (g ~ 1e-20 gives
     # g*g ~ 1e-40), squares that overflow to inf (|g| >= 2e19), exact zeros and
     # signed tiny values must round exactly as the oracle's do
     import torch
 
     n, P = 4, 4096
-    pair = Pair(n, P, "ring", "f32", gamma=0.1, precisions=("f32",))
+    pair = Pair(n, P, "ring", dtype, gamma=0.1, precisions=("f32",))
     rng = np.random.default_rng(21)
     specials = np.array([0.0, -0.0, 1e-20, -3e-21, 1e-38, 3e-39, -7e-45, 1e19, -2e19, 3e20, 1e-3, -5.0],
                         dtype=np.float32)
@@ -561,4 +562,4 @@ def test_extreme_gradients_bit_exact():
         pair.gossip_round(t)
     stats = pair.check_state(tag="extreme gradients")
     log("bit-exact fraction vs fp32 oracle: %s" % stats)
-    assert np.isfinite(pair.gather("x")).all()
+    assert np.isfinite(pair.params_f64(pair.gather("x"))).all()
