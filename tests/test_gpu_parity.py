@@ -563,3 +563,20 @@ def test_extreme_gradients_bit_exact(dtype):
     stats = pair.check_state(tag="extreme gradients")
     log("bit-exact fraction vs fp32 oracle: %s" % stats)
     assert np.isfinite(pair.params_f64(pair.gather("x"))).all()
+
+
+def test_two_contexts_interleaved_stay_independent():
+    # two contexts on the same device, different graphs, dtypes and kernels
+    # (n=8 phase kernel, n=40 slot-reusing kernel), rounds interleaved
+    a = Pair(8, 9_001, "exponential", "f32", gamma=0.1, precisions=("f32",))
+    b = Pair(40, 7_003, "one_peer", "bf16", gamma=0.2, precisions=("f32",))
+    for t in range(3):
+        a.local_step()
+        b.local_step()
+        b.local_step()
+        a.gossip_round(t)
+        b.local_step_gossip_round(t)
+        reduction_close(a.gpu.consensus_error(), a.oracles["f32"].consensus_error(), "context a round %d" % t)
+        reduction_close(b.gpu.consensus_error(), b.oracles["f32"].consensus_error(), "context b round %d" % t)
+    a.check_state(tag="context a")
+    b.check_state(tag="context b")
