@@ -4,6 +4,8 @@ Importable by the tests, the smoke check and the benchmark's CPU-baseline leg.
 The GPU library (paper_2606_11081_amd) never imports it.
 """
 from .oracle import (  # noqa: F401
+    PARAM_BF16,
+    PARAM_NATIVE,
     Oracle,
     OracleHParams,
     TOPOLOGY_CODES,

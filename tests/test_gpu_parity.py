@@ -502,6 +502,26 @@ def test_maximum_row_length_64bit_offsets():
     torch.cuda.empty_cache()
 
 
+def host_consensus_error(x, n, P, param_dtype, chunk=1 << 23):
+    """The oracle's two-pass fp64 consensus error of the whole stored x,
+    downloaded column chunk by column chunk (the sum is additive over columns)."""
+    import ctypes
+
+    import torch
+
+    L = oracle.lib("f32")
+    code = oracle.PARAM_BF16 if param_dtype == "bf16" else oracle.PARAM_NATIVE
+    total = 0.0
+    for c0 in range(0, P, chunk):
+        c1 = min(P, c0 + chunk)
+        part = x[:, c0:c1].contiguous()
+        host = (part.view(torch.int16).cpu().numpy().view(np.uint16) if param_dtype == "bf16"
+                else part.cpu().numpy())
+        host = np.ascontiguousarray(host)
+        total += L.orc_consensus_error(n, c1 - c0, c1 - c0, code, host.ctypes.data_as(ctypes.c_void_p))
+    return total
+
+
 @pytest.mark.parametrize("name,sample,rounds", FULL)
 def test_full_size_sampled(name, sample, rounds):
     import torch
@@ -531,6 +551,10 @@ def test_full_size_sampled(name, sample, rounds):
         reduction_close(head, o.consensus_error(slice(0, 64)), "%s round %d CE head" % (name, t))
         reduction_close(tail, o.consensus_error(slice(len(cols) - 64, len(cols))), "%s CE tail" % name)
         log("round %d: CE %.6e" % (t, fused))
+    # the fused full-size CE of the last round against the oracle's definition
+    # over the whole downloaded state
+    whole_host = host_consensus_error(pair.gpu.x, w.n, w.P, w.param_dtype)
+    assert abs(whole_host - fused) <= 1e-9 * whole_host, (whole_host, fused)
     stats = pair.check_state(tag=name)
     log("bit-exact fraction vs fp32 oracle: %s" % stats)
     del pair
