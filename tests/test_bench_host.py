@@ -1,0 +1,121 @@
+"""Host-side logic of bench.py, on the CPU: the algorithmic byte counts that
+price every kernel against the HBM roofline, the one-GPU guard, the parser of
+the committed PMC summaries and the oracle-timing leg."""
+import importlib.util
+import os
+import re
+import subprocess
+import sys
+
+import pytest
+
+import gasloc_inputs as gi
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def bench():
+    spec = importlib.util.spec_from_file_location("bench_under_test", os.path.join(ROOT, "bench.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def moved(reads, writes):
+    return sum(reads.values()) + sum(writes.values())
+
+
+@pytest.mark.parametrize("sp", [4, 2])
+def test_adamw_bytes_are_the_buffers_it_streams(bench, sp):
+    # one local step (Sec. 2, the inner AdamW update): params, grads and both
+    # moments are read; params and moments written back; grads stay fp32
+    assert bench.adamw_bytes_per_rp(sp) == moved({"y": sp, "g": 4, "m": 4, "v": 4},
+                                                  {"y": sp, "m": 4, "v": 4})
+
+
+@pytest.mark.parametrize("sp", [4, 2])
+@pytest.mark.parametrize("gamma", [0.0, 0.1])
+@pytest.mark.parametrize("stepped", [True, False])
+@pytest.mark.parametrize("with_u", [True, False])
+def test_gossip_bytes_are_the_buffers_it_streams(bench, sp, gamma, stepped, with_u):
+    # Eq. 1 / Eq. 2: x, the local iterate y (only if the worker stepped),
+    # the outer momentum u (mu != 0) and the previous z (gamma != 0) are read;
+    # x, u and the stored z are written
+    reads = {"x": sp}
+    writes = {"x": sp}
+    if stepped:
+        reads["y"] = sp
+    if with_u:
+        reads["u"] = writes["u"] = 4
+    if gamma:
+        reads["zp"] = writes["zp"] = 4
+    assert bench.gossip_bytes_per_rp(sp, gamma, stepped=stepped, with_u=with_u) == moved(reads, writes)
+
+
+@pytest.mark.parametrize("sp", [4, 2])
+def test_fused_bytes_add_the_last_step_without_its_iterate(bench, sp):
+    # the fused last step reads g, m, v and writes m, v; its new iterate only
+    # feeds the pseudo-gradient, so it is neither stored nor re-read
+    for gamma in (0.0, 0.1):
+        for stepped in (True, False):
+            base = bench.gossip_bytes_per_rp(sp, gamma, stepped=stepped)
+            assert bench.fused_bytes_per_rp(sp, gamma, True, stepped) == base + 4 + 8 + 8
+            assert bench.fused_bytes_per_rp(sp, gamma, False, stepped) == base
+
+
+@pytest.mark.parametrize("name, gossip_gb, adamw_gb", [
+    ("exp-n8-p124m", 27.776, 27.776),
+    ("onepeer-exp-n16-p350m", 156.8, 156.8),
+    ("regular3-n32-p150m-bf16", 105.6, 115.2),
+    ("matching-n64-p50m-hetH", 64.0, 89.6),
+])
+def test_bytes_per_round_of_the_workloads(bench, name, gossip_gb, adamw_gb):
+    w = gi.WORKLOADS[name]
+    sp = bench.param_bytes(w.param_dtype)
+    assert w.n * w.P * bench.gossip_bytes_per_rp(sp, w.gamma) == pytest.approx(gossip_gb * 1e9, rel=1e-12)
+    assert w.n * w.P * bench.adamw_bytes_per_rp(sp) == pytest.approx(adamw_gb * 1e9, rel=1e-12)
+
+
+def test_default_workload_is_the_n16_p350m_configuration(bench):
+    w = gi.WORKLOADS[bench.DEFAULT_WORKLOAD]
+    assert (w.n, w.P, w.topology, w.param_dtype, w.H, w.gamma) == (16, 350_000_000, "one_peer_exp", "f32", 10, 0.1)
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode != 0
+    assert "one GPU" in r.stderr and "2 requested" in r.stderr
+    assert r.stdout == ""
+
+
+def test_committed_pmc_summaries_parse(bench):
+    names = [f for f in os.listdir(os.path.join(ROOT, "profiles")) if f.endswith("_pmc.md")]
+    assert names
+    for f in names:
+        text = open(os.path.join(ROOT, "profiles", f)).read()
+        m = re.search(r"traffic_bytes_per_dispatch:\s*([0-9.eE+]+)\s+kernels_sha:\s*([0-9a-f]{16})\b", text)
+        assert m, f
+        assert float(m.group(1)) > 0
+        assert "rocprofv3 --pmc FETCH_SIZE" in text and "rocprofv3 --pmc WRITE_SIZE" in text, f
+
+
+def test_traffic_is_withheld_for_another_kernel_source(bench, tmp_path, monkeypatch):
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    (prof / "k_local_adamw_w_pmc.md").write_text("traffic_bytes_per_dispatch: 1.5e+11 kernels_sha: 0123456789abcdef\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernels_sha", lambda: "0123456789abcdef")
+    assert bench.read_traffic("k_local_adamw", "w") == 1.5e11
+    monkeypatch.setattr(bench, "kernels_sha", lambda: "fedcba9876543210")
+    assert bench.read_traffic("k_local_adamw", "w") is None
+    assert bench.read_traffic("missing", "w") is None
+
+
+def test_cpu_baseline_times_the_oracle_on_a_sample(bench):
+    w = gi.WORKLOADS[bench.DEFAULT_WORKLOAD]
+    out = bench.cpu_baseline(w, gi.local_steps(w), 2000)
+    assert out["kind"] == "oracle" and out["cores"] == 1
+    assert out["unit"] == "replica-param updates/s" and out["value"] > 0
+    assert "2000 of 350000000 columns x 16 workers" in out["sample"]
