@@ -18,13 +18,17 @@ bool make_topology(const gasloc_topology& topo, int n, uint64_t t, int32_t* row_
                    float* val, int32_t cap, int32_t* nnz, std::string* err);
 // Visit plan of a round for the slot-reusing kernel (plan.cpp): super-steps
 // of at most kPlanBatch new z values and at most kPlanRows rows; the plan is
-// checked by verify_plan before it is returned.
+// checked by verify_plan before it is returned.  With reuse_mix, a row whose
+// CSR entries equal those of the row summed just before it is encoded with
+// kPlanReuseMix in place of its entry count and takes that row's sum (only
+// for round forms whose neighbour sum does not depend on the row itself).
 constexpr int kPlanBatch = 4;
 constexpr int kPlanRows = 4;
-bool plan_round(int n, const int32_t* rp, const int32_t* col, const float* val, std::vector<int32_t>* ops,
-                int* slots_used, std::string* err);
-bool verify_plan(int n, const int32_t* rp, const int32_t* col, const float* val, const int32_t* ops, int len,
-                 int slots, std::string* err);
+constexpr int32_t kPlanReuseMix = -1;
+bool plan_round(int n, const int32_t* rp, const int32_t* col, const float* val, bool reuse_mix,
+                std::vector<int32_t>* ops, int* slots_used, std::string* err);
+bool verify_plan(int n, const int32_t* rp, const int32_t* col, const float* val, bool reuse_mix,
+                 const int32_t* ops, int len, int slots, std::string* err);
 // Upper bound on the words of a plan for n workers.
 size_t plan_words_max(int n);
 bool skip_exchanges(int n, const int32_t* rp, const int32_t* col, const float* val, const uint8_t* alive,

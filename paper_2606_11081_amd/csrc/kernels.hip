@@ -304,9 +304,9 @@ __global__ __launch_bounds__(256) void k_local_adamw(AdamArgs a) {
 
 // ---------------------------------------------------------------------------
 // a2-a5: pseudo-gradient, outer step, neighbour mix, consensus momentum, and
-// the consensus-error and squared-pseudo-gradient partials, fused.  A thread owns V consecutive columns
-// of *every* worker, so each element of x, y, u, zp is read and written
-// exactly once and the in-place updates cannot race.  Phase 1 puts one value
+// the consensus-error and squared-pseudo-gradient partials, fused.  A thread
+// owns V consecutive columns of *every* worker, so each element of x, y, u,
+// zp is read and written exactly once and the in-place updates cannot race.  Phase 1 puts one value
 // per worker in this thread's private LDS slots (no barrier is needed
 // between writing and gathering them); phase 2 gathers the neighbours of
 // each row through the CSR, which is staged in LDS once per workgroup.
@@ -587,7 +587,8 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
 //
 // Plan words: [S, start_0 .. start_{S-1}], super-step at start_s:
 //   npre, nrows, (worker, slot) x npre, row x nrows,
-//   then per row: nent, own_slot, (slot, weight bits) x nent.
+//   then per row: nent, own_slot, (slot, weight bits) x nent, or
+//   kPlanReuseMix, own_slot (EQ, DAdam: the previous summed row's sum).
 // ---------------------------------------------------------------------------
 
 typedef const __attribute__((address_space(4))) int32_t plan_word;
@@ -721,12 +722,15 @@ __device__ __forceinline__ void planned_issue(const GossipArgs& a, plan_word* op
 
 // Running consensus-error sums of one column group (shifted by its first
 // stored row, as in k_gossip_round); `fresh` until that row is stored.  pg:
-// this thread's running sum of squared pseudo-gradients x_i - y_i.
+// this thread's running sum of squared pseudo-gradients x_i - y_i.  mix: the
+// neighbour sum of the last row that summed its entries, taken by the rows
+// the plan marks kPlanReuseMix.
 template <int V>
 struct CeSums {
   double shift[V], s[V], q[V];
   bool fresh;
   double pg;
+  float mix[V];
 };
 
 template <int DT, int V, int R, bool FUSED, int FORM, bool TAIL>
@@ -819,6 +823,8 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
   //   ALG1:        d = sum_k W_rk (x_r - y_k), outer step from x_r
   //   DAdam:       x_r = sum_k W_rk x_k + (y_r - x_r)
   //   Local-DAdam: d = sum_k W_rk (x_r - x_k), outer step from y_r
+  // In EQ and DAdam the sum does not depend on the row, so a row with the
+  // entries of the row summed before it takes that sum (kPlanReuseMix).
   const int rows_at = at + 2 + 2 * npre;
   int pos = rows_at + nrows;
 #pragma unroll
@@ -842,14 +848,17 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
       for (int c = 0; c < V; ++c) xi[c] = own[c];
     }
     constexpr bool kDiff = kAlg1 || FORM == GASLOC_FORM_LOCAL_DADAM;
+    // a reusing row starts from the kept sum and adds no entries
+    const bool reuse = !kDiff && nent == kPlanReuseMix;
+    const int count = reuse ? 0 : nent;
     float acc[V];
 #pragma unroll
-    for (int c = 0; c < V; ++c) acc[c] = 0.0f;
-    for (int k0 = 0; k0 < nent; k0 += 4) {
+    for (int c = 0; c < V; ++c) acc[c] = reuse ? cs.mix[c] : 0.0f;
+    for (int k0 = 0; k0 < count; k0 += 4) {
       float zk[4][V], wk[4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        if (k0 + t >= nent) break;
+        if (k0 + t >= count) break;
         const float* src = mine + ops[pos + 2 + 2 * (k0 + t)] * slot_stride;
         wk[t] = __int_as_float(ops[pos + 3 + 2 * (k0 + t)]);
 #pragma unroll
@@ -857,12 +866,16 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
       }
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        if (k0 + t >= nent) break;
+        if (k0 + t >= count) break;
 #pragma unroll
         for (int c = 0; c < V; ++c) acc[c] = acc[c] + wk[t] * (kDiff ? xi[c] - zk[t][c] : zk[t][c]);
       }
     }
-    pos += 2 + 2 * nent;
+    pos += 2 + 2 * count;
+    if constexpr (!kDiff) {
+#pragma unroll
+      for (int c = 0; c < V; ++c) cs.mix[c] = acc[c];
+    }
     float res[V];
     if constexpr (kEq) {
       if (a.apply_gamma) {
@@ -1032,9 +1045,9 @@ __device__ __forceinline__ void load_cols(const void* base, int64_t idx, int lo,
 // A thread takes a group of columns of every worker (4 fp32 or 8 bf16, i.e.
 // 16 bytes; groups are aligned so every row's vector loads are, and the
 // groups at the ends of the range are masked), with the loads of 8 workers
-// (fp32) or 4 (bf16, twice the columns; 8 left it register-bound) in flight.  Per column
-// the sums are those of the fused kernel: shifted by worker 0's value, fp64,
-// workers in order.
+// (fp32) or 4 (bf16, twice the columns; 8 left it register-bound) in
+// flight.  Per column the sums are those of the fused kernel: shifted by
+// worker 0's value, fp64, workers in order.
 template <int DT>
 __global__ __launch_bounds__(256) void k_consensus_error(const void* x, int64_t ld, int n,
                                                          int64_t p_begin, int64_t p_end,

@@ -12,9 +12,17 @@
 // order of every row, is that of the phase kernel; only independent work is
 // reordered.
 //
+// Rows with the same CSR entries (columns and weight bits) have bit-identical
+// neighbour sums.  When the round form's sum does not depend on the row itself
+// (reuse_mix), such rows follow the first of them directly and take its sum:
+// every row of the complete graph, the second row of every 1-Peer pair.  A
+// follower must hold its own index among those columns, so its own value is
+// live when it is emitted.
+//
 // Encoding (int32): [S, start_0 .. start_{S-1}], and at start_s super-step s:
 //   n_pre, n_rows, (worker, slot) x n_pre, row x n_rows,
-//   then per row: n_ent, own_slot, (slot, weight bits) x n_ent
+//   then per row: n_ent, own_slot, (slot, weight bits) x n_ent,
+//   or kPlanReuseMix, own_slot for a row that takes the last summed row's sum
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
@@ -27,9 +35,44 @@ namespace gasloc {
 
 namespace {
 
+bool same_entries(const int32_t* rp, const int32_t* col, const float* val, int a, int b) {
+  const int32_t len = rp[a + 1] - rp[a];
+  if (rp[b + 1] - rp[b] != len) return false;
+  for (int32_t k = 0; k < len; ++k) {
+    if (col[rp[a] + k] != col[rp[b] + k]) return false;
+    if (std::memcmp(&val[rp[a] + k], &val[rp[b] + k], sizeof(float)) != 0) return false;
+  }
+  return true;
+}
+
+bool has_column(const int32_t* rp, const int32_t* col, int row, int j) {
+  return std::binary_search(col + rp[row], col + rp[row + 1], j);
+}
+
+// twins[i]: the other rows with row i's CSR entries that hold their own
+// index among them, i.e. the rows that can follow i and take its sum.
+std::vector<std::vector<int>> find_twins(int n, const int32_t* rp, const int32_t* col, const float* val) {
+  std::vector<std::vector<int>> twins(static_cast<size_t>(n));
+  std::vector<char> grouped(static_cast<size_t>(n), 0);
+  for (int i = 0; i < n; ++i) {
+    if (grouped[static_cast<size_t>(i)]) continue;
+    std::vector<int> group{i};
+    for (int r = i + 1; r < n; ++r)
+      if (!grouped[static_cast<size_t>(r)] && same_entries(rp, col, val, i, r)) {
+        group.push_back(r);
+        grouped[static_cast<size_t>(r)] = 1;
+      }
+    for (int lead : group)
+      for (int r : group)
+        if (r != lead && has_column(rp, col, r, r)) twins[static_cast<size_t>(lead)].push_back(r);
+  }
+  return twins;
+}
+
 // One greedy plan starting from row `first`.
-void greedy_plan(int n, const int32_t* rp, const int32_t* col, const float* val, int first,
-                 std::vector<int32_t>* ops, int* slots_used) {
+void greedy_plan(int n, const int32_t* rp, const int32_t* col, const float* val,
+                 const std::vector<std::vector<int>>& twins, int first, std::vector<int32_t>* ops,
+                 int* slots_used) {
   constexpr int max_pre = kPlanBatch, max_rows = kPlanRows;
   // need[i]: columns of row i plus i itself, ascending
   std::vector<std::vector<int>> need(static_cast<size_t>(n));
@@ -43,16 +86,27 @@ void greedy_plan(int n, const int32_t* rp, const int32_t* col, const float* val,
     for (int j : nd) ++uses[static_cast<size_t>(j)];
   }
   std::vector<int> slot_of(static_cast<size_t>(n), -1);
-  std::vector<char> emitted(static_cast<size_t>(n), 0);
+  std::vector<char> emitted(static_cast<size_t>(n), 0), follows(static_cast<size_t>(n), 0);
   std::vector<int> free_slots;  // sorted descending: back() is the lowest free slot
   int high = 0, done = 0;
   std::vector<int32_t> body;
   std::vector<int32_t> starts;
   std::vector<int> rows, pres;
+  std::vector<int> queue;  // followers still to emit, in order
+  size_t queued = 0;
   while (done < n) {
     rows.clear();
     pres.clear();
     for (;;) {
+      if (queued < queue.size()) {  // followers go right after their leader
+        if (static_cast<int>(rows.size()) >= max_rows) break;
+        const int r = queue[queued++];
+        rows.push_back(r);
+        emitted[static_cast<size_t>(r)] = 1;
+        follows[static_cast<size_t>(r)] = 1;
+        ++done;
+        continue;
+      }
       // next row: fewest new z to compute minus slots it frees; ties -> the
       // row with more of its z already live, then the lowest index
       int best = -1, best_cost = 1 << 30, best_new = 0, best_live = -1;
@@ -98,6 +152,10 @@ void greedy_plan(int n, const int32_t* rp, const int32_t* col, const float* val,
       rows.push_back(best);
       emitted[static_cast<size_t>(best)] = 1;
       ++done;
+      queue.clear();
+      queued = 0;
+      for (int r : twins[static_cast<size_t>(best)])
+        if (!emitted[static_cast<size_t>(r)]) queue.push_back(r);
     }
     // a row that alone needs more than kPlanBatch new z values gets super-steps
     // of its first values with no rows before it
@@ -120,6 +178,11 @@ void greedy_plan(int n, const int32_t* rp, const int32_t* col, const float* val,
     }
     for (int r : rows) body.push_back(r);
     for (int r : rows) {
+      if (follows[static_cast<size_t>(r)]) {
+        body.push_back(kPlanReuseMix);
+        body.push_back(slot_of[static_cast<size_t>(r)]);
+        continue;
+      }
       body.push_back(rp[r + 1] - rp[r]);
       body.push_back(slot_of[static_cast<size_t>(r)]);
       for (int32_t k = rp[r]; k < rp[r + 1]; ++k) {
@@ -151,9 +214,11 @@ size_t plan_words_max(int n) {
   return 1 + 6 * m + 5 * m + 2 * m * m;
 }
 
-bool plan_round(int n, const int32_t* rp, const int32_t* col, const float* val, std::vector<int32_t>* ops,
-                int* slots_used, std::string* err) {
-  greedy_plan(n, rp, col, val, 0, ops, slots_used);
+bool plan_round(int n, const int32_t* rp, const int32_t* col, const float* val, bool reuse_mix,
+                std::vector<int32_t>* ops, int* slots_used, std::string* err) {
+  const std::vector<std::vector<int>> twins =
+      reuse_mix ? find_twins(n, rp, col, val) : std::vector<std::vector<int>>(static_cast<size_t>(n));
+  greedy_plan(n, rp, col, val, twins, 0, ops, slots_used);
   // graphs with many live values at once: try a few other first rows and
   // keep the plan that needs the fewest slots (deterministic choice)
   if (*slots_used > 8) {
@@ -161,24 +226,26 @@ bool plan_round(int n, const int32_t* rp, const int32_t* col, const float* val, 
     int trial_slots = 0;
     const int tries = std::min(n, 8);
     for (int t = 1; t < tries; ++t) {
-      greedy_plan(n, rp, col, val, t * n / tries, &trial, &trial_slots);
+      greedy_plan(n, rp, col, val, twins, t * n / tries, &trial, &trial_slots);
       if (trial_slots < *slots_used) {
         ops->swap(trial);
         *slots_used = trial_slots;
       }
     }
   }
-  return verify_plan(n, rp, col, val, ops->data(), static_cast<int>(ops->size()), *slots_used, err);
+  return verify_plan(n, rp, col, val, reuse_mix, ops->data(), static_cast<int>(ops->size()), *slots_used, err);
 }
 
 // Replays a plan symbolically: the start table points at consecutive
 // super-steps that tile the words after it; every slot read holds the worker
 // the CSR names; every z is computed exactly once before use; every row is
-// emitted exactly once with its CSR entries in order; slots stay within
-// `slots`; super-steps hold at most kPlanRows rows and kPlanBatch new z, and
-// a super-step without rows is followed by one that has some.
-bool verify_plan(int n, const int32_t* rp, const int32_t* col, const float* val, const int32_t* ops, int len,
-                 int slots, std::string* err) {
+// emitted exactly once with its CSR entries in order, or (reuse_mix only) as
+// taking the sum of the last row summed before it, whose CSR entries it
+// shares; slots stay within `slots`; super-steps hold at most kPlanRows rows
+// and kPlanBatch new z, and a super-step without rows is followed by one that
+// has some.
+bool verify_plan(int n, const int32_t* rp, const int32_t* col, const float* val, bool reuse_mix,
+                 const int32_t* ops, int len, int slots, std::string* err) {
   auto bad = [&](const char* what) {
     *err = std::string("round plan: ") + what;
     return false;
@@ -187,7 +254,7 @@ bool verify_plan(int n, const int32_t* rp, const int32_t* col, const float* val,
   const int supers = ops[0];
   std::vector<int> holder(static_cast<size_t>(slots), -1);
   std::vector<char> computed(static_cast<size_t>(n), 0), emitted(static_cast<size_t>(n), 0);
-  int pc = 1 + supers, rows_seen = 0;
+  int pc = 1 + supers, rows_seen = 0, last_summed = -1;
   for (int s = 0; s < supers; ++s) {
     if (ops[1 + s] != pc || pc + 2 > len) return bad("super-step start");
     const int npre = ops[pc], nrows = ops[pc + 1];
@@ -208,8 +275,15 @@ bool verify_plan(int n, const int32_t* rp, const int32_t* col, const float* val,
       if (r < 0 || r >= n || emitted[static_cast<size_t>(r)] || pc + 2 > len) return bad("row id");
       const int nent = ops[pc], own = ops[pc + 1];
       pc += 2;
-      if (nent != rp[r + 1] - rp[r] || pc + 2 * nent > len) return bad("row header");
       if (own < 0 || own >= slots || holder[static_cast<size_t>(own)] != r) return bad("own slot");
+      if (nent == kPlanReuseMix) {
+        if (!reuse_mix || last_summed < 0 || !same_entries(rp, col, val, last_summed, r)) return bad("reused sum");
+        emitted[static_cast<size_t>(r)] = 1;
+        ++rows_seen;
+        continue;
+      }
+      if (nent != rp[r + 1] - rp[r] || pc + 2 * nent > len) return bad("row header");
+      last_summed = r;
       for (int e = 0; e < nent; ++e) {
         const int slot = ops[pc++];
         int32_t bits;

@@ -288,19 +288,21 @@ gasloc_status upload_plan(gasloc_ctx* c, const std::vector<int32_t>& ops) {
 }
 
 // Which kernel runs a round: the phase kernel keeps every worker's slot
-// value in LDS; the planned kernel (plan.cpp) keeps only the live ones.
-// Measured on MI355X (EQ form): planned is 2.3x faster at n=64 (1-Peer) and
-// 1.9x at n=32 (3-regular), where LDS limits the phase kernel; at n <= 16 the
-// phase kernel fits and keeps more loads in flight (fused round at n=16: 45.0
-// vs 48.2 ms), and a dense W needs a slot per worker anyway.
+// value in LDS; the planned kernel (plan.cpp) keeps only the live ones and
+// lets rows with equal entries share one neighbour sum.  Measured on MI355X
+// (EQ form, gossip round alone): beyond 16 workers planned is faster on every
+// graph (n=64: 1-Peer 15.0 vs 28.2 ms, complete 34.5 vs 247 ms; n=32:
+// 3-regular 1.9x, complete 28.8 vs 74.8 ms) or tied (n=64 exponential); at
+// n <= 16 the phase kernel keeps more loads in flight and the two tie, except
+// the fused round (n=16 one-peer exponential: 44.8 vs 45.4 ms) and the
+// complete graph (n=16: 29.8 vs 26.1 ms).
 // Override for tuning sweeps: GASLOC_GOSSIP_KERNEL=phase|planned.
-enum class KernelChoice { kPhase, kPlanned, kBySlots };
-KernelChoice kernel_choice(const gasloc_ctx& c) {
+bool use_planned_kernel(const gasloc_ctx& c) {
   if (const char* env = std::getenv("GASLOC_GOSSIP_KERNEL")) {
-    if (std::strcmp(env, "phase") == 0) return KernelChoice::kPhase;
-    if (std::strcmp(env, "planned") == 0) return KernelChoice::kPlanned;
+    if (std::strcmp(env, "phase") == 0) return false;
+    if (std::strcmp(env, "planned") == 0) return true;
   }
-  return c.n > 16 ? KernelChoice::kBySlots : KernelChoice::kPhase;
+  return c.n > 16;
 }
 
 gasloc_status reduce_cols(gasloc_ctx* c, int64_t p0, int64_t p1) {
@@ -398,14 +400,15 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
     val = c->skip_val.data();
   }
   DeviceGuard guard(c->device);
-  bool planned = false;
+  const bool planned = use_planned_kernel(*c);
   int slots = 0;
-  const KernelChoice choice = kernel_choice(*c);
-  if (choice != KernelChoice::kPhase) {
+  if (planned) {
+    // rows with equal entries share their neighbour sum where it does not
+    // depend on the row (EQ, DAdam)
+    const bool reuse_mix = c->hp.round_form == GASLOC_FORM_EQ || c->hp.round_form == GASLOC_FORM_DADAM;
     std::string err;
-    if (!gasloc::plan_round(c->n, rp, col, val, &c->plan_ops, &slots, &err))
+    if (!gasloc::plan_round(c->n, rp, col, val, reuse_mix, &c->plan_ops, &slots, &err))
       return fail(c, GASLOC_EINVAL, err);
-    planned = choice == KernelChoice::kPlanned || slots < c->n;
   }
   gasloc::LaunchShape shape;
   size_t lds = 0;
@@ -557,9 +560,10 @@ gasloc_status gasloc_init(int32_t n, int64_t P, const gasloc_topology* topology,
   c->alive.assign(static_cast<size_t>(n), 1);
   if (topology->admissible) {
     c->admissible.assign(topology->admissible, topology->admissible + static_cast<size_t>(n) * n);
+    auto edge = [&](int i, int j) { return c->admissible[static_cast<size_t>(i) * n + j] != 0; };
     for (int i = 0; i < n; ++i)
       for (int j = 0; j < n; ++j)
-        if ((c->admissible[static_cast<size_t>(i) * n + j] != 0) != (c->admissible[static_cast<size_t>(j) * n + i] != 0)) {
+        if (edge(i, j) != edge(j, i)) {
           delete c;
           return fail(nullptr, GASLOC_EINVAL, "the admissible graph must be symmetric");
         }

@@ -12,11 +12,11 @@ extern "C" {
 
 // Plans W (CSR, n rows); writes at most cap words to out.  Returns the word
 // count, or -1 with the message in err (size err_cap).
-int plan_shim_plan(int n, const int32_t* rp, const int32_t* col, const float* val, int32_t* out, int cap,
-                   int* slots, char* err, int err_cap) {
+int plan_shim_plan(int n, const int32_t* rp, const int32_t* col, const float* val, int reuse_mix, int32_t* out,
+                   int cap, int* slots, char* err, int err_cap) {
   std::vector<int32_t> ops;
   std::string e;
-  if (!gasloc::plan_round(n, rp, col, val, &ops, slots, &e)) {
+  if (!gasloc::plan_round(n, rp, col, val, reuse_mix != 0, &ops, slots, &e)) {
     std::snprintf(err, static_cast<size_t>(err_cap), "%s", e.c_str());
     return -1;
   }
@@ -28,11 +28,13 @@ int plan_shim_plan(int n, const int32_t* rp, const int32_t* col, const float* va
   return static_cast<int>(ops.size());
 }
 
-int plan_shim_verify(int n, const int32_t* rp, const int32_t* col, const float* val, const int32_t* ops, int len,
-                     int slots) {
+int plan_shim_verify(int n, const int32_t* rp, const int32_t* col, const float* val, int reuse_mix,
+                     const int32_t* ops, int len, int slots) {
   std::string e;
-  return gasloc::verify_plan(n, rp, col, val, ops, len, slots, &e) ? 1 : 0;
+  return gasloc::verify_plan(n, rp, col, val, reuse_mix != 0, ops, len, slots, &e) ? 1 : 0;
 }
+
+int plan_shim_reuse_code() { return gasloc::kPlanReuseMix; }
 
 int64_t plan_shim_words_max(int n) { return static_cast<int64_t>(gasloc::plan_words_max(n)); }
 

@@ -3,11 +3,13 @@
 
 The planner reorders a round's independent work: each worker's slot value is
 computed once into an LDS slot before its first reader and the slot is
-reused after its last reader.  Here every plan is replayed numerically the
-way the kernel consumes it (slots as an array, rows summed in the order the
-plan lists their entries) and must reproduce sum_k W_ik z_k in CSR order
-bit for bit, with every row emitted once; tampered plans must be rejected
-by the planner's own verifier.
+reused after its last reader; with reuse allowed, a row whose CSR entries
+equal those of the row summed just before it takes that sum.  Here every
+plan is replayed numerically the way the kernel consumes it (slots as an
+array, rows summed in the order the plan lists their entries, a reusing row
+taking the last sum) and must reproduce sum_k W_ik z_k in CSR order bit for
+bit, with every row emitted once; tampered plans must be rejected by the
+planner's own verifier.
 """
 import ctypes
 import os
@@ -36,9 +38,10 @@ def shim(tmp_path_factory):
     lib = ctypes.CDLL(out)
     P = ctypes.POINTER
     lib.plan_shim_plan.argtypes = [ctypes.c_int, P(ctypes.c_int32), P(ctypes.c_int32), P(ctypes.c_float),
-                                   P(ctypes.c_int32), ctypes.c_int, P(ctypes.c_int), ctypes.c_char_p, ctypes.c_int]
+                                   ctypes.c_int, P(ctypes.c_int32), ctypes.c_int, P(ctypes.c_int), ctypes.c_char_p,
+                                   ctypes.c_int]
     lib.plan_shim_verify.argtypes = [ctypes.c_int, P(ctypes.c_int32), P(ctypes.c_int32), P(ctypes.c_float),
-                                     P(ctypes.c_int32), ctypes.c_int, ctypes.c_int]
+                                     ctypes.c_int, P(ctypes.c_int32), ctypes.c_int, ctypes.c_int]
     lib.plan_shim_words_max.restype = ctypes.c_int64
     return lib
 
@@ -47,7 +50,7 @@ def _ptr(a, t):
     return a.ctypes.data_as(ctypes.POINTER(t))
 
 
-def plan(lib, n, rp, col, val):
+def plan(lib, n, rp, col, val, reuse=False):
     rp, col, val = (np.ascontiguousarray(rp, np.int32), np.ascontiguousarray(col, np.int32),
                     np.ascontiguousarray(val, np.float32))
     cap = int(lib.plan_shim_words_max(n))
@@ -55,23 +58,26 @@ def plan(lib, n, rp, col, val):
     slots = ctypes.c_int(0)
     err = ctypes.create_string_buffer(256)
     k = lib.plan_shim_plan(n, _ptr(rp, ctypes.c_int32), _ptr(col, ctypes.c_int32), _ptr(val, ctypes.c_float),
-                           _ptr(out, ctypes.c_int32), cap, ctypes.byref(slots), err, 256)
+                           int(reuse), _ptr(out, ctypes.c_int32), cap, ctypes.byref(slots), err, 256)
     assert k > 0, err.value.decode()
     return out[:k].copy(), slots.value
 
 
-def verify(lib, n, rp, col, val, ops, slots):
+def verify(lib, n, rp, col, val, ops, slots, reuse=False):
     rp, col, val = (np.ascontiguousarray(rp, np.int32), np.ascontiguousarray(col, np.int32),
                     np.ascontiguousarray(val, np.float32))
     ops = np.ascontiguousarray(ops, np.int32)
     return lib.plan_shim_verify(n, _ptr(rp, ctypes.c_int32), _ptr(col, ctypes.c_int32), _ptr(val, ctypes.c_float),
-                                _ptr(ops, ctypes.c_int32), len(ops), slots) == 1
+                                int(reuse), _ptr(ops, ctypes.c_int32), len(ops), slots) == 1
 
 
-def replay(lib, n, rp, col, val, ops, slots, z):
+def replay(lib, n, rp, col, val, ops, slots, z, reuse=False):
     """Runs the plan on slot values z (float32 [n]) as the kernel does and
-    returns the row sums; asserts the plan's structural limits on the way."""
-    batch, rows_max = lib.plan_shim_batch(), lib.plan_shim_rows()
+    returns the row sums and the rows that took the previous sum; asserts
+    the plan's structural limits on the way."""
+    batch, rows_max, reuse_code = lib.plan_shim_batch(), lib.plan_shim_rows(), lib.plan_shim_reuse_code()
+    reused = []
+    last = None  # (row, sum) of the last row that summed its entries
     S = int(ops[0])
     assert 1 <= S <= 2 * n
     lds = np.full(slots, np.nan, np.float32)
@@ -97,6 +103,18 @@ def replay(lib, n, rp, col, val, ops, slots, z):
             nent, own = int(ops[pc]), int(ops[pc + 1])
             pc += 2
             assert holder[own] == r, "own slot of row %d" % r
+            assert not done[r]
+            done[r] = True
+            if nent == reuse_code:
+                assert reuse and last is not None
+                lr = last[0]
+                assert np.array_equal(col[rp[r]:rp[r + 1]], col[rp[lr]:rp[lr + 1]])
+                assert np.array_equal(np.asarray(val[rp[r]:rp[r + 1]], np.float32).view(np.uint32),
+                                      np.asarray(val[rp[lr]:rp[lr + 1]], np.float32).view(np.uint32))
+                out[r] = last[1]
+                reused.append(r)
+                continue
+            assert nent == rp[r + 1] - rp[r]
             acc = np.float32(0.0)
             for k in range(nent):
                 sl, bits = int(ops[pc]), int(ops[pc + 1])
@@ -104,11 +122,10 @@ def replay(lib, n, rp, col, val, ops, slots, z):
                 w = np.array([bits], np.int32).view(np.float32)[0]
                 assert holder[sl] == col[rp[r] + k] and w == val[rp[r] + k]
                 acc = np.float32(acc + np.float32(w * lds[sl]))
-            assert not done[r]
-            done[r] = True
             out[r] = acc
+            last = (r, acc)
     assert pc == len(ops) and done.all()
-    return out
+    return out, reused
 
 
 def dense_order_sums(n, rp, col, val, z):
@@ -121,33 +138,54 @@ def dense_order_sums(n, rp, col, val, z):
     return out
 
 
-def check(lib, n, rp, col, val, seed=0):
-    ops, slots = plan(lib, n, rp, col, val)
+def check(lib, n, rp, col, val, seed=0, reuse=False):
+    ops, slots = plan(lib, n, rp, col, val, reuse)
     assert 1 <= slots <= n
     assert len(ops) <= lib.plan_shim_words_max(n)
     z = np.random.default_rng(seed).standard_normal(n).astype(np.float32)
-    got = replay(lib, n, rp, col, val, ops, slots, z)
+    got, reused = replay(lib, n, rp, col, val, ops, slots, z, reuse)
     assert np.array_equal(got.view(np.uint32), dense_order_sums(n, rp, col, val, z).view(np.uint32))
-    assert verify(lib, n, rp, col, val, ops, slots)
-    return ops, slots
+    assert verify(lib, n, rp, col, val, ops, slots, reuse)
+    if reused:
+        assert not verify(lib, n, rp, col, val, ops, slots, False)
+    return ops, slots, sorted(reused)
 
 
 KINDS = ["ring", "complete", "exponential", "one_peer_exp", "one_peer", "two_peer", "random_regular"]
 
 
+def rows_with_an_equal_earlier_row(n, rp, col, val):
+    seen, count = set(), 0
+    for i in range(n):
+        key = (tuple(col[rp[i]:rp[i + 1]]), np.asarray(val[rp[i]:rp[i + 1]], np.float32).tobytes())
+        count += key in seen
+        seen.add(key)
+    return count
+
+
+@pytest.mark.parametrize("reuse", [False, True])
 @pytest.mark.parametrize("kind", KINDS)
 @pytest.mark.parametrize("n", [1, 2, 5, 16, 17, 32, 33, 64])
-def test_generated_graphs_replay_exactly(shim, kind, n):
+def test_generated_graphs_replay_exactly(shim, kind, n, reuse):
     if kind == "random_regular" and (n <= 3 or (3 * n) % 2):
         pytest.skip("3-regular graph needs n > 3 and 3n even")
     for t in range(6):
         rp, col, val = oracle.topology_csr(kind, n, 3, t, 3)
-        ops, slots = check(shim, n, rp, col, val, seed=t)
+        ops, slots, reused = check(shim, n, rp, col, val, seed=t, reuse=reuse)
         if kind in ("one_peer", "ring") and n >= 16:
             assert slots <= 8, (kind, n, slots)  # sparse graphs reuse slots
+        # the generated graphs carry every self-loop, so every row equal to an
+        # earlier one can take its sum: all but one row of the complete graph,
+        # one row of each 1-Peer pair
+        assert len(reused) == (rows_with_an_equal_earlier_row(n, rp, col, val) if reuse else 0)
+        if reuse and kind == "complete":
+            assert len(reused) == n - 1
+        if reuse and kind == "one_peer":
+            assert len(reused) == n // 2
 
 
-def test_random_csrs_with_dense_rows_and_missing_diagonals(shim):
+@pytest.mark.parametrize("reuse", [False, True])
+def test_random_csrs_with_dense_rows_and_missing_diagonals(shim, reuse):
     rng = np.random.default_rng(11)
     for trial in range(300):
         n = int(rng.integers(1, 65))
@@ -161,20 +199,46 @@ def test_random_csrs_with_dense_rows_and_missing_diagonals(shim):
         rp = np.concatenate([[0], np.cumsum([len(c) for c in rows])]).astype(np.int32)
         col = np.concatenate(rows).astype(np.int32)
         val = np.concatenate([np.full(len(c), 1.0 / len(c)) for c in rows]).astype(np.float32)
-        check(shim, n, rp, col, val, seed=trial)
+        check(shim, n, rp, col, val, seed=trial, reuse=reuse)
 
 
-def test_tampered_plans_are_rejected(shim):
+def test_equal_rows_without_their_own_column_sum_their_entries(shim):
+    # four equal rows reading workers 2 and 3: rows 0 and 1 cannot take an
+    # earlier row's sum (their own values are not among those columns, so
+    # they may not be live), rows 2 and 3 follow whichever row sums first
+    rp = np.array([0, 2, 4, 6, 8], np.int32)
+    col = np.array([2, 3, 2, 3, 2, 3, 2, 3], np.int32)
+    val = np.full(8, 0.5, np.float32)
+    ops, slots, reused = check(shim, 4, rp, col, val, reuse=True)
+    assert reused == [2, 3]
+
+
+@pytest.mark.parametrize("kind, reuse", [("two_peer", False), ("one_peer", True), ("complete", True)])
+def test_tampered_plans_are_rejected(shim, kind, reuse):
     n = 12
-    rp, col, val = oracle.topology_csr("two_peer", n, 5, 2)
-    ops, slots = check(shim, n, rp, col, val)
+    rp, col, val = oracle.topology_csr(kind, n, 5, 2)
+    ops, slots, reused = check(shim, n, rp, col, val, reuse=reuse)
+    assert bool(reused) == reuse
     rejected = 0
     for k in range(len(ops)):
         for d in (-1, 1, 1000):
             bad = ops.copy()
             bad[k] += d
-            rejected += not verify(shim, n, rp, col, val, bad, slots)
+            rejected += not verify(shim, n, rp, col, val, bad, slots, reuse)
     assert rejected == 3 * len(ops)
-    assert not verify(shim, n, rp, col, val, ops[:-1], slots)
-    assert not verify(shim, n, rp, col, val, ops, slots - 1)
+    assert not verify(shim, n, rp, col, val, ops[:-1], slots, reuse)
+    assert not verify(shim, n, rp, col, val, ops, slots - 1, reuse)
+
+
+def test_reused_sum_needs_equal_entries(shim):
+    n = 6
+    rp, col, val = oracle.topology_csr("complete", n, 0, 0)
+    ops, slots, reused = check(shim, n, rp, col, val, reuse=True)
+    assert len(reused) == n - 1
+    # the same plan against a CSR whose later rows differ in one weight bit
+    for r in range(n):
+        other = np.asarray(val, np.float32).copy()
+        k = rp[r] + r % (rp[r + 1] - rp[r])
+        other[k] = np.nextafter(other[k], np.float32(1.0))
+        assert not verify(shim, n, rp, col, other, ops, slots, True), r
 
