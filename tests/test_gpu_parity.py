@@ -79,6 +79,9 @@ SMALL = [
     (33, 515, "two_peer", "f32", 1, 0.3, 0.5, True),
     (64, 2053, "complete", "f32", 1, 0.0, 0.9, True),
     (64, 4099, "one_peer", "bf16", 2, 0.0, 0.9, True),
+    # n > 16, rows sharing one neighbour sum, with the consensus-momentum term
+    (40, 3333, "complete", "f32", 2, 0.1, 0.9, True),
+    (34, 2049, "one_peer", "bf16", 1, 0.2, 0.5, False),
     (7, 3, "ring", "f32", 1, 0.1, 0.9, True),
     (4, 1, "complete", "bf16", 1, 0.1, 0.9, True),
 ]
@@ -108,6 +111,7 @@ FUSED = [
     (8, 65_537, "exponential", "bf16", 2, 0.1),
     (64, 20_011, "one_peer", "f32", 2, 0.0),
     (33, 9_999, "two_peer", "bf16", 1, 0.2),
+    (40, 7_001, "complete", "bf16", 2, 0.1),
 ]
 
 
@@ -162,6 +166,10 @@ FORMS = [
     ("alg1", 24, 9_001, "random_regular", "bf16", 1, 0.9, False),
     ("dadam", 48, 7_777, "one_peer_exp", "f32", 2, 0.9, True),
     ("local_dadam", 33, 6_007, "exponential", "bf16", 2, 0.9, True),
+    # complete graph beyond 16 workers: shared sums (DAdam) and n live slots
+    # without them (ALG1, the DiLoCo reduction)
+    ("dadam", 40, 5_003, "complete", "bf16", 2, 0.9, True),
+    ("alg1", 40, 4_001, "complete", "f32", 2, 0.0, True),
 ]
 
 
