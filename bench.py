@@ -112,6 +112,19 @@ def cpu_baseline(w, H_i, columns):
                       % (columns, w.P, w.n, int(H_i.max()), host_cpu(), os.cpu_count() or 0, dt)}
 
 
+# Oracle work units (one worker-column through one local step or one gossip
+# round) in the default CPU sample: about 12 s on one core of the MI355X host,
+# 30M columns of the n=16, H=10 workload.
+CPU_SAMPLE_UNITS = 30_000_000 * 16 * 11
+
+
+def cpu_sample_columns(w, H_i):
+    """Columns of the oracle's sample: a fixed amount of work whatever the
+    workload's worker count and local steps, at most the whole row."""
+    per_column = w.n * (float(H_i.mean()) + 1.0)
+    return int(max(1, min(w.P, CPU_SAMPLE_UNITS // per_column)))
+
+
 def host_cpu():
     try:
         with open("/proc/cpuinfo") as f:
@@ -129,7 +142,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--cpu-columns", type=int, default=30_000_000)
+    ap.add_argument("--cpu-columns", type=int, default=0,
+                    help="columns of the oracle's sample (0: sized to about 12 s of single-core work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-gb", type=float, default=8.0, help="size of the copy probe (GB read)")
     ap.add_argument("--no-fuse", dest="fuse", action="store_false",
@@ -295,8 +309,9 @@ def main():
     del grads
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
-        log("bench: timing the oracle on %d columns" % args.cpu_columns)
-        out["cpu_baseline"] = cpu_baseline(w, H_i, min(args.cpu_columns, w.P))
+        columns = min(args.cpu_columns, w.P) if args.cpu_columns > 0 else cpu_sample_columns(w, H_i)
+        log("bench: timing the oracle on %d columns" % columns)
+        out["cpu_baseline"] = cpu_baseline(w, H_i, columns)
     print(json.dumps(out), flush=True)
 
 

@@ -119,3 +119,17 @@ def test_cpu_baseline_times_the_oracle_on_a_sample(bench):
     assert out["kind"] == "oracle" and out["cores"] == 1
     assert out["unit"] == "replica-param updates/s" and out["value"] > 0
     assert "2000 of 350000000 columns x 16 workers" in out["sample"]
+
+
+def test_cpu_sample_is_a_fixed_amount_of_work(bench):
+    sizes = {}
+    for name, w in gi.WORKLOADS.items():
+        H_i = gi.local_steps(w)
+        cols = bench.cpu_sample_columns(w, H_i)
+        assert 1 <= cols <= w.P
+        sizes[name] = cols
+        if cols < w.P:  # work = columns x workers x (local steps + the round)
+            work = cols * w.n * (H_i.mean() + 1)
+            assert abs(work - bench.CPU_SAMPLE_UNITS) <= w.n * (H_i.mean() + 1)
+    assert sizes["onepeer-exp-n16-p350m"] == 30_000_000
+    assert sizes["ring-n4-p1m"] == 1_048_576  # the whole row
