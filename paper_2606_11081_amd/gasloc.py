@@ -352,8 +352,13 @@ class GASLoC:
         raise AttributeError(name)
 
     def set_params(self, x0):
-        """Identical start: every worker's x is x0 (torch tensor of length P)."""
-        self.bufs["x"][:, : self.P].copy_(x0.to(self.bufs["x"].dtype).view(1, -1).expand(self.n, -1))
+        """Identical start: every worker's x is x0 (torch tensor of length P),
+        written on the context's stream so that later calls see it."""
+        import torch
+
+        self.stream.wait_stream(torch.cuda.current_stream(self.stream.device))  # x0 may come from there
+        with torch.cuda.stream(self.stream):
+            self.bufs["x"][:, : self.P].copy_(x0.to(self.bufs["x"].dtype).view(1, -1).expand(self.n, -1))
 
     def local_step(self, grads, lr, active=None):
         gasloc_local_step(self.ctx, grads, grads.shape[1], active, lr)

@@ -612,3 +612,45 @@ def test_two_contexts_interleaved_stay_independent():
         reduction_close(b.gpu.consensus_error(), b.oracles["f32"].consensus_error(), "context b round %d" % t)
     a.check_state(tag="context a")
     b.check_state(tag="context b")
+
+
+def test_context_on_a_side_stream_matches_the_oracle():
+    # every call enqueues on the context's stream: a context made on a side
+    # stream (default priority) and fed from that stream gives the oracle's bits
+    import torch
+
+    import paper_2606_11081_amd as g
+
+    n, P = 6, 5_003
+    side = torch.cuda.Stream()
+    gpu = g.GASLoC(n, P, topology="two_peer", seed=gi.SEED_TOPOLOGY, stream=side, beta1=gi.BETA1,
+                   beta2=gi.BETA2, eps=gi.EPS, weight_decay=gi.WEIGHT_DECAY, outer_lr=gi.OUTER_LR,
+                   outer_momentum=gi.OUTER_MOMENTUM, consensus_momentum=0.1)
+    hp = oracle.OracleHParams(beta1=gi.BETA1, beta2=gi.BETA2, eps=gi.EPS, weight_decay=gi.WEIGHT_DECAY,
+                              outer_lr=gi.OUTER_LR, outer_momentum=gi.OUTER_MOMENTUM, consensus_momentum=0.1)
+    ref = oracle.Oracle(n, P, hp, topology="two_peer", seed=gi.SEED_TOPOLOGY, precision="f32")
+    x0 = gi.make_x0(P, device="cuda")  # made on the current stream
+    gpu.set_params(x0)
+    ref.set_params(x0.cpu().numpy())
+    grads = torch.empty((n, gpu.ld), dtype=torch.float32, device="cuda")
+    mu = gi.worker_means(n)
+    for t in range(3):
+        with torch.cuda.stream(side):
+            gi.fill_grads(grads, mu, t)
+            gpu.local_step(grads, gi.LOCAL_LR)
+            if t == 2:
+                gpu.local_step_gossip_round(grads, gi.LOCAL_LR, t)
+            else:
+                gpu.gossip_round(t)
+        side.synchronize()
+        g_host = grads[:, :P].cpu().numpy()
+        ref.local_step(g_host, gi.LOCAL_LR)
+        if t == 2:
+            ref.local_step(g_host, gi.LOCAL_LR)
+        ref.gossip_round(t)
+        reduction_close(gpu.consensus_error(), ref.consensus_error(), "side stream round %d" % t)
+    side.synchronize()
+    for name in ("x", "m", "v", "u", "zp"):
+        got = getattr(gpu, name)[:, :P].cpu().numpy()
+        assert np.array_equal(got.view(np.uint32), getattr(ref, name).view(np.uint32)), name
+    gpu.close()
