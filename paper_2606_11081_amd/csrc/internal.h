@@ -118,6 +118,8 @@ size_t planned_lds_bytes(int slots, const LaunchShape& shape);
 hipError_t launch_consensus_error(const void* x, int dtype, int64_t ld, int n, int64_t p_begin,
                                   int64_t p_end, double* partials, int blocks, hipStream_t stream);
 hipError_t launch_finalize(const double* partials, int count, double* out, hipStream_t stream);
+// out[0] = sum of a[0..count), out[1] = sum of b[0..count), each as launch_finalize sums.
+hipError_t launch_finalize2(const double* a, const double* b, int count, double* out, hipStream_t stream);
 hipError_t launch_replica_mean(const void* x, int dtype, int64_t ld, int n, int64_t P, void* out,
                                int blocks, hipStream_t stream);
 

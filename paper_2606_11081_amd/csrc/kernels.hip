@@ -1107,6 +1107,22 @@ __global__ __launch_bounds__(256) void k_finalize(const double* partials, int co
   if (threadIdx.x == 0) *out = total;
 }
 
+// The same for the two partial arrays of a round (consensus error, squared
+// pseudo-gradients) in one launch: out[0], out[1], each in k_finalize's order.
+__global__ __launch_bounds__(256) void k_finalize2(const double* a, const double* b, int count, double* out) {
+  double va = 0.0, vb = 0.0;
+  for (int k = threadIdx.x; k < count; k += blockDim.x) {
+    va += a[k];
+    vb += b[k];
+  }
+  double ta, tb;
+  block_sum2(va, vb, ta, tb);
+  if (threadIdx.x == 0) {
+    out[0] = ta;
+    out[1] = tb;
+  }
+}
+
 // a6: network average, fp64 sum in worker order, rounded to the param dtype;
 // 16 bytes of columns per thread, the loads of 8 workers in flight at a time.
 template <int DT>
@@ -1294,6 +1310,11 @@ hipError_t launch_consensus_error(const void* x, int dtype, int64_t ld, int n, i
 
 hipError_t launch_finalize(const double* partials, int count, double* out, hipStream_t stream) {
   hipLaunchKernelGGL(k_finalize, dim3(1), dim3(256), 0, stream, partials, count, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_finalize2(const double* a, const double* b, int count, double* out, hipStream_t stream) {
+  hipLaunchKernelGGL(k_finalize2, dim3(1), dim3(256), 0, stream, a, b, count, out);
   return hipGetLastError();
 }
 

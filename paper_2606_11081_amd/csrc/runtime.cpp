@@ -9,8 +9,10 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <initializer_list>
 #include <new>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "gasloc.h"
@@ -72,7 +74,8 @@ struct gasloc_ctx {
   bool ce_current = false;        // d_ce holds the consensus error of the stored x
   bool failed = false;
 
-  unsigned char* d_csr = nullptr;  // device copy of the round's CSR
+  unsigned char* d_csr = nullptr;  // device copy of the round's CSR or visit plan
+  std::vector<unsigned char> d_csr_key;  // what d_csr holds (kind byte + contents), to skip repeats
   unsigned char* h_stage[kStageSlots] = {};
   hipEvent_t stage_done[kStageSlots] = {};
   bool stage_used[kStageSlots] = {};
@@ -254,9 +257,37 @@ void release(gasloc_ctx* c) {
   delete c;
 }
 
-// Copies a CSR into the next pinned slot and enqueues its upload to d_csr.
+// True if d_csr already holds `parts` (a kind byte, then the contents); else
+// records them as what d_csr is about to hold.  A static graph (or plan) is
+// then uploaded once, not every round.
+using ByteSpan = std::pair<const void*, size_t>;
+bool already_uploaded(gasloc_ctx* c, unsigned char kind, std::initializer_list<ByteSpan> parts) {
+  size_t len = 1;
+  for (const auto& p : parts) len += p.second;
+  bool same = c->d_csr_key.size() == len && c->d_csr_key[0] == kind;
+  size_t at = 1;
+  for (const auto& p : parts) {
+    if (!same) break;
+    same = std::memcmp(c->d_csr_key.data() + at, p.first, p.second) == 0;
+    at += p.second;
+  }
+  if (same) return true;
+  c->d_csr_key.assign(1, kind);
+  for (const auto& p : parts) {
+    const unsigned char* b = static_cast<const unsigned char*>(p.first);
+    c->d_csr_key.insert(c->d_csr_key.end(), b, b + p.second);
+  }
+  return false;
+}
+
+// Copies a CSR into the next pinned slot and enqueues its upload to d_csr
+// (nothing if d_csr already holds it).
 gasloc_status upload_csr(gasloc_ctx* c, const int32_t* row_ptr, const int32_t* col, const float* val,
                          int nnz) {
+  if (already_uploaded(c, 'C', {{row_ptr, sizeof(int32_t) * static_cast<size_t>(c->n + 1)},
+                                {col, sizeof(int32_t) * static_cast<size_t>(nnz)},
+                                {val, sizeof(float) * static_cast<size_t>(nnz)}}))
+    return GASLOC_OK;
   const int slot = c->stage_next;
   c->stage_next = (c->stage_next + 1) % kStageSlots;
   if (c->stage_used[slot]) HIP_TRY(c, hipEventSynchronize(c->stage_done[slot]));
@@ -272,10 +303,12 @@ gasloc_status upload_csr(gasloc_ctx* c, const int32_t* row_ptr, const int32_t* c
   return GASLOC_OK;
 }
 
-// Copies a visit plan into the next pinned slot and enqueues its upload.
+// Copies a visit plan into the next pinned slot and enqueues its upload
+// (nothing if d_csr already holds it).
 gasloc_status upload_plan(gasloc_ctx* c, const std::vector<int32_t>& ops) {
   if (sizeof(int32_t) * ops.size() > plan_stage_bytes(c->n))
     return fail(c, GASLOC_EINVAL, "round plan larger than its staging buffer");
+  if (already_uploaded(c, 'P', {{ops.data(), sizeof(int32_t) * ops.size()}})) return GASLOC_OK;
   const int slot = c->stage_next;
   c->stage_next = (c->stage_next + 1) % kStageSlots;
   if (c->stage_used[slot]) HIP_TRY(c, hipEventSynchronize(c->stage_done[slot]));
@@ -504,8 +537,7 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
     HIP_TRY(c, gasloc::launch_gossip_round(a, c->hp.param_dtype, step != nullptr, c->hp.round_form, shape,
                                            c->stream));
   }
-  HIP_TRY(c, gasloc::launch_finalize(c->d_partials, shape.blocks, c->d_ce, c->stream));
-  HIP_TRY(c, gasloc::launch_finalize(a.pg_partials, shape.blocks, c->d_ce + 1, c->stream));
+  HIP_TRY(c, gasloc::launch_finalize2(c->d_partials, a.pg_partials, shape.blocks, c->d_ce, c->stream));
   if (step) {
     for (int i = 0; i < c->n; ++i)
       if ((step->active >> i) & 1ull) c->k[static_cast<size_t>(i)] += 1;

@@ -336,6 +336,39 @@ def test_explicit_random_csr_large_n(density, dtype):
     pair.check_state(tag="explicit n=40 density %g" % density)
 
 
+def _csr_from_rows(rows):
+    rp = np.zeros(len(rows) + 1, np.int32)
+    cols, vals = [], []
+    for i, (c, w) in enumerate(rows):
+        cols += list(c)
+        vals += list(w)
+        rp[i + 1] = len(cols)
+    return rp, np.array(cols, np.int32), np.array(vals, np.float32)
+
+
+@pytest.mark.parametrize("form,dtype", [("eq", "f32"), ("eq", "bf16"), ("dadam", "f32")])
+def test_explicit_csr_with_equal_rows(form, dtype):
+    # groups of rows with equal entries at n = 24: rows 0-5 all read workers
+    # 0-5 (each holds its own column: five of them take the first one's sum);
+    # rows 6-9 all read workers 8 and 9 (rows 6 and 7 lack their own column,
+    # so only rows 8 and 9 may take another row's sum); the rest are distinct
+    n, P = 24, 12_007
+    rng = np.random.default_rng(5 + (dtype == "bf16") + 2 * (form == "dadam"))
+    pair = Pair(n, P, "ring", dtype, gamma=0.1 if form == "eq" else 0.0, form=form)
+    for t in range(3):
+        pair.local_step()
+        w6 = rng.random(6) + 0.1
+        w2 = rng.random(2) + 0.1
+        rows = [(range(6), w6 / w6.sum())] * 6 + [((8, 9), w2 / w2.sum())] * 4
+        for i in range(10, n):
+            c = sorted({i, (i + 1 + t) % n, (i + 5) % n})
+            w = rng.random(len(c)) + 0.1
+            rows.append((c, w / w.sum()))
+        pair.gossip_round(t, W=_csr_from_rows(rows))
+        reduction_close(pair.gpu.consensus_error(), pair.oracles["f32"].consensus_error(), "CE round %d" % t)
+    pair.check_state(tag="equal rows %s %s" % (form, dtype))
+
+
 def test_all_inactive_step_changes_nothing():
     import torch
 
