@@ -284,7 +284,9 @@ def main():
         "ms_per_step": round(ms_step, 3),
         "round_ms_p10_p50_p90": [round(float(np.percentile(wall, q)), 3) for q in (10, 50, 90)],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": w.param_dtype, "data": "synthetic",
+        # the arithmetic of every kernel is fp32 (reductions fp64), whatever the
+        # parameters are stored in; the storage type is config.param_dtype
+        "dtype": "f32", "data": "synthetic",
         "config": {"workload": w.name, "n": w.n, "P": w.P, "topology": w.topology,
                    "local_steps": "U{%d..%d}" % w.hetero_H if w.hetero_H else w.H,
                    "gamma": w.gamma, "param_dtype": w.param_dtype, "state_dtype": "f32",
