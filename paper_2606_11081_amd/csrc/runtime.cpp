@@ -660,11 +660,13 @@ gasloc_status gasloc_init(int32_t n, int64_t P, const gasloc_topology* topology,
 
   if ((e = hipMemsetAsync(c->d_ce, 0, 2 * sizeof(double), c->stream)) != hipSuccess)
     return init_fail(e, "hipMemsetAsync");
-  // zero the optimizer state of every worker: m, v, u, zp
-  const size_t state_bytes = sizeof(float) * static_cast<size_t>(n) * static_cast<size_t>(b.ld);
+  // zero the optimizer state of every worker, m, v, u, zp: columns [0, P) of
+  // each row only (the row padding is the caller's)
   for (float* p : {b.m, b.v, b.u, b.zp}) {
     if (!p) continue;
-    if ((e = hipMemsetAsync(p, 0, state_bytes, c->stream)) != hipSuccess) return init_fail(e, "hipMemsetAsync");
+    if ((e = hipMemset2DAsync(p, sizeof(float) * static_cast<size_t>(b.ld), 0, sizeof(float) * static_cast<size_t>(P),
+                              static_cast<size_t>(n), c->stream)) != hipSuccess)
+      return init_fail(e, "hipMemset2DAsync");
   }
   *out = c;
   return GASLOC_OK;

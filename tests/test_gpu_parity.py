@@ -687,3 +687,68 @@ def test_context_on_a_side_stream_matches_the_oracle():
         got = getattr(gpu, name)[:, :P].cpu().numpy()
         assert np.array_equal(got.view(np.uint32), getattr(ref, name).view(np.uint32)), name
     gpu.close()
+
+
+@pytest.mark.parametrize("n,topology,dtype,form", [
+    (8, "exponential", "f32", "eq"),       # phase kernel
+    (24, "one_peer", "bf16", "eq"),        # planned kernel, rows sharing sums
+    (40, "complete", "f32", "dadam"),
+    (33, "two_peer", "bf16", "alg1"),
+])
+def test_row_padding_is_never_touched(n, topology, dtype, form):
+    # columns p >= P of every buffer (and of the gradients and the mean's
+    # output) hold a NaN canary through init, local steps, fused and plain
+    # rounds and every reduction: none is written, and none leaks into the
+    # stored values
+    import torch
+
+    from paper_2606_11081_amd import gasloc as gl
+
+    P = 4_099
+    ld = gl.padded_ld(P, dtype) + 96
+    gld = ld + 40
+    canary32, canary16 = 0x7FC0DEAD, 0x7FCD
+    pdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+
+    def filled(shape, dt):
+        t = torch.empty(shape, dtype=dt, device="cuda")
+        if dt == torch.bfloat16:
+            t.view(torch.int16).fill_(canary16)
+        else:
+            t.view(torch.int32).fill_(canary32)
+        return t
+
+    x, y = filled((n, ld), pdt), filled((n, ld), pdt)
+    m, v, u, zp = (filled((n, ld), torch.float32) for _ in range(4))
+    grads = filled((n, gld), torch.float32)
+    mean = filled((P + 64,), pdt)
+    gamma = 0.1 if form == "eq" else 0.0
+    x[:, :P] = gi.make_x0(P, device="cuda").to(pdt)
+    hp = gl.make_hparams(param_dtype=dtype, round_form=form, consensus_momentum=gamma)
+    stream = torch.cuda.current_stream()
+    ctx = gl.gasloc_init(n, P, gl.make_topology_struct(topology, gi.SEED_TOPOLOGY, 3), hp, x, y, m, v, u, zp, ld,
+                         stream.cuda_stream)
+    try:
+        mu = gi.worker_means(n)
+        for t in range(3):
+            gi.fill_grads(grads[:, :P], mu, t)
+            gl.gasloc_local_step(ctx, grads, gld, None, gi.LOCAL_LR)
+            if form in ("eq", "alg1") and t != 1:
+                gl.gasloc_local_step_gossip_round(ctx, grads, gld, None, gi.LOCAL_LR, None, t)
+            else:
+                gl.gasloc_gossip_round(ctx, None, t)
+            assert np.isfinite(gl.gasloc_consensus_error(ctx))
+            assert np.isfinite(gl.gasloc_pseudo_gradient_sq(ctx))
+            gl.gasloc_consensus_error_cols(ctx, 1, P)
+            gl.gasloc_replica_mean(ctx, mean)
+        torch.cuda.synchronize()
+    finally:
+        gl.gasloc_destroy(ctx)
+    for name, buf in (("x", x), ("y", y), ("m", m), ("v", v), ("u", u), ("zp", zp), ("grads", grads)):
+        pad = buf[:, P:]
+        bits = pad.view(torch.int16) if buf.dtype == torch.bfloat16 else pad.view(torch.int32)
+        want = canary16 if buf.dtype == torch.bfloat16 else canary32
+        assert bool((bits == want).all()), "%s: row padding written" % name
+    tail = mean[P:].view(torch.int16) if dtype == "bf16" else mean[P:].view(torch.int32)
+    assert bool((tail == (canary16 if dtype == "bf16" else canary32)).all()), "mean: padding written"
+    assert bool(torch.isfinite(x[:, :P].float()).all()) and bool(torch.isfinite(mean[:P].float()).all())
