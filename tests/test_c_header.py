@@ -40,3 +40,22 @@ def test_plain_c_consumer(tmp_path):
     f = lambda v: float(np.float32(v))  # the C program passes float arguments
     expect = [oracle.lr_schedule(f(1e-3), s, 100, f(0.1), f(0.01), 0.0) for s in (0, 10, 99)]
     assert [np.float32(v) for v in lr] == [np.float32(v) for v in expect]
+
+
+@pytest.mark.gpu
+def test_c_program_runs_rounds_on_the_gpu(tmp_path):
+    # whole rounds through the C ABI from a C program (hipMalloc'd buffers, no
+    # Python or torch in that process), bit-identical to the fp32 oracle
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    exe = str(tmp_path / "c_device_consumer")
+    subprocess.run([cc, "-std=c11", "-Wall", "-Wextra", "-Werror", "-O2", "-ffp-contract=off", "-D__HIP_PLATFORM_AMD__",
+                    "-I" + os.path.join(ROOT, "include"), "-I" + os.path.join(rocm, "include"),
+                    os.path.join(ROOT, "tests", "c_device_consumer.c"), os.path.join(ROOT, "oracle", "gasloc_oracle.c"),
+                    "-L" + LIBDIR, "-lgasloc", "-Wl,-rpath," + LIBDIR, "-L" + os.path.join(rocm, "lib"), "-lamdhip64",
+                    "-Wl,-rpath," + os.path.join(rocm, "lib"), "-lm", "-o", exe], check=True, capture_output=True)
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "c_device_consumer: ok" in r.stdout
