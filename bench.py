@@ -49,22 +49,30 @@ def adamw_bytes_per_rp(sp):
     return 2 * sp + 20
 
 
-def gossip_bytes_per_rp(sp, gamma, stepped=True, with_u=True):
-    # read x, y (stepped workers), u, zp (gamma); write x, u, zp (gamma)
+FORMS = ("eq", "alg1", "dadam", "local_dadam")
+
+
+def gossip_bytes_per_rp(sp, gamma, stepped=True, with_u=True, form="eq"):
+    """Algorithmic bytes of one round per replica-parameter.
+    eq:          read x, y (stepped workers), u, zp (gamma); write x, u, zp (gamma)
+    alg1:        read x, y (x again for a worker that did not step), u; write x, u
+    dadam:       read x, y (stepped workers); write x (no outer momentum)
+    local_dadam: read x, y (stepped workers), u; write x, u"""
     b = sp + sp  # x read + x write
-    if stepped:
+    if stepped or form == "alg1":
         b += sp
-    if with_u:
+    if with_u and form != "dadam":
         b += 8
-    if gamma != 0.0:
+    if gamma != 0.0 and form == "eq":
         b += 8
     return b
 
 
-def fused_bytes_per_rp(sp, gamma, active, stepped, with_u=True):
-    """Fused last local step + round, per worker: an active worker also reads
-    g, m, v and writes m, v; its new iterate is never stored."""
-    b = gossip_bytes_per_rp(sp, gamma, stepped=stepped, with_u=with_u)
+def fused_bytes_per_rp(sp, gamma, active, stepped, with_u=True, form="eq"):
+    """Fused last local step + round (EQ and ALG1), per worker: an active
+    worker also reads g, m, v and writes m, v; its new iterate is never
+    stored."""
+    b = gossip_bytes_per_rp(sp, gamma, stepped=stepped, with_u=with_u, form=form)
     if active:
         b += 4 + 8 + 8
     return b
@@ -83,9 +91,10 @@ def read_traffic(kernel, workload):
     return float(m.group(1))
 
 
-def cpu_baseline(w, H_i, columns):
+def cpu_baseline(w, H_i, columns, form="eq"):
     """The oracle as it stands, single-threaded, on `columns` columns of the
-    same workload: one full round (all local steps, gossip, consensus error)."""
+    same workload: one full round (all local steps, gossip, consensus error)
+    in the same round form."""
     import numpy as np
 
     import gasloc_inputs as gi
@@ -93,7 +102,7 @@ def cpu_baseline(w, H_i, columns):
 
     hp = oracle.OracleHParams(beta1=gi.BETA1, beta2=gi.BETA2, eps=gi.EPS, weight_decay=gi.WEIGHT_DECAY,
                               outer_lr=gi.OUTER_LR, outer_momentum=gi.OUTER_MOMENTUM,
-                              nesterov=True, consensus_momentum=w.gamma)
+                              nesterov=True, consensus_momentum=w.gamma if form == "eq" else 0.0, form=form)
     o = oracle.Oracle(w.n, columns, hp, topology=w.topology, seed=gi.SEED_TOPOLOGY, degree=w.degree,
                       precision="f32", param_dtype=w.param_dtype)
     rng = np.random.default_rng(0)
@@ -107,9 +116,10 @@ def cpu_baseline(w, H_i, columns):
     o.consensus_error()
     dt = time.perf_counter() - t0
     return {"value": w.n * columns / dt, "unit": "replica-param updates/s", "cores": 1, "kind": "oracle",
-            "sample": "%d of %d columns x %d workers, one round (%d local steps + gossip + CE), "
+            "sample": "%d of %d columns x %d workers, one round (%d local steps + %s round + CE), "
                       "plain C oracle (fp32 build, -O2, single thread on %s, %d host threads visible): %.2f s"
-                      % (columns, w.P, w.n, int(H_i.max()), host_cpu(), os.cpu_count() or 0, dt)}
+                      % (columns, w.P, w.n, int(H_i.max()), form.upper() if form == "eq" else form, host_cpu(),
+                         os.cpu_count() or 0, dt)}
 
 
 # Oracle work units (one worker-column through one local step or one gossip
@@ -148,7 +158,11 @@ def main():
     ap.add_argument("--copy-gb", type=float, default=8.0, help="size of the copy probe (GB read)")
     ap.add_argument("--no-fuse", dest="fuse", action="store_false",
                     help="run the last local step and the round as two calls")
+    ap.add_argument("--form", choices=FORMS, default="eq",
+                    help="round form (non-EQ forms run with gamma = 0; DAdam forms without the fused step)")
     args = ap.parse_args()
+    if args.form in ("dadam", "local_dadam"):
+        args.fuse = False
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: every replica of the round lives on a single MI355X; "
@@ -162,18 +176,21 @@ def main():
     import paper_2606_11081_amd as g
 
     w = gi.WORKLOADS[args.workload]
+    gamma = w.gamma if args.form == "eq" else 0.0  # the consensus momentum exists in EQ only
+    # profiles and the JSON name the workload with its round form when not EQ
+    wname = w.name if args.form == "eq" else "%s-%s" % (w.name, args.form)
     H_i = gi.local_steps(w)
     masks = gi.active_masks(H_i)
     sp = param_bytes(w.param_dtype)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    log("bench: %s  (n=%d P=%d %s H=%s gamma=%g)" % (w.name, w.n, w.P, w.param_dtype,
-                                                    "U{%d..%d}" % w.hetero_H if w.hetero_H else w.H, w.gamma))
+    log("bench: %s  (n=%d P=%d %s H=%s gamma=%g)" % (wname, w.n, w.P, w.param_dtype,
+                                                    "U{%d..%d}" % w.hetero_H if w.hetero_H else w.H, gamma))
 
     lib = g.GASLoC(w.n, w.P, topology=w.topology, seed=gi.SEED_TOPOLOGY, degree=w.degree,
                    param_dtype=w.param_dtype, beta1=gi.BETA1, beta2=gi.BETA2, eps=gi.EPS,
                    weight_decay=gi.WEIGHT_DECAY, outer_lr=gi.OUTER_LR, outer_momentum=gi.OUTER_MOMENTUM,
-                   outer_nesterov=True, consensus_momentum=w.gamma)
+                   outer_nesterov=True, consensus_momentum=gamma, round_form=args.form)
     lib.set_params(gi.make_x0(w.P, device=dev))
     # one resident gradient batch (stand-in for backpropagated gradients)
     grads = torch.empty((w.n, lib.ld), dtype=torch.float32, device=dev)
@@ -230,10 +247,10 @@ def main():
         act_last = masks[-1]
         # a worker read y in the fused call if it took a local step earlier this round
         stepped_before = np.minimum(H_i, len(masks) - 1) > 0
-        round_bytes = sum(fused_bytes_per_rp(sp, w.gamma, bool(act_last[i]), bool(stepped_before[i]))
+        round_bytes = sum(fused_bytes_per_rp(sp, gamma, bool(act_last[i]), bool(stepped_before[i]), form=args.form)
                           for i in range(w.n)) * w.P
     else:
-        round_bytes = w.n * w.P * gossip_bytes_per_rp(sp, w.gamma)
+        round_bytes = w.n * w.P * gossip_bytes_per_rp(sp, gamma, form=args.form)
     adam_gbps = sum(r * adam_bytes for r in adam_rp) / (sum(adam_ms) * 1e-3) / 1e9 if adam_ms else 0.0
     round_gbps = round_bytes / (np.mean(round_ms) * 1e-3) / 1e9
     adam_total, round_total = sum(adam_ms), sum(round_ms)
@@ -247,7 +264,7 @@ def main():
         e[1].record(stream)
         torch.cuda.synchronize()
         g_ms.append(e[0].elapsed_time(e[1]))
-    gossip_bytes = gossip_bytes_per_rp(sp, w.gamma)
+    gossip_bytes = gossip_bytes_per_rp(sp, gamma, form=args.form)
     gossip_ms = float(np.median(g_ms))
     gossip_gbps = w.n * w.P * gossip_bytes / (gossip_ms * 1e-3) / 1e9
 
@@ -274,7 +291,7 @@ def main():
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
-                "traffic": read_traffic(dom, w.name),
+                "traffic": read_traffic(dom, wname),
                 "algorithmic_bytes_per_launch": int(dom_bytes), "avg_launch_ms": round(dom_ms, 4)}
     out = {
         "metric": METRIC,
@@ -287,16 +304,16 @@ def main():
         # the arithmetic of every kernel is fp32 (reductions fp64), whatever the
         # parameters are stored in; the storage type is config.param_dtype
         "dtype": "f32", "data": "synthetic",
-        "config": {"workload": w.name, "n": w.n, "P": w.P, "topology": w.topology,
+        "config": {"workload": wname, "n": w.n, "P": w.P, "topology": w.topology, "round_form": args.form,
                    "local_steps": "U{%d..%d}" % w.hetero_H if w.hetero_H else w.H,
-                   "gamma": w.gamma, "param_dtype": w.param_dtype, "state_dtype": "f32",
+                   "gamma": gamma, "param_dtype": w.param_dtype, "state_dtype": "f32",
                    "last_local_step_fused": bool(args.fuse)},
         "roofline": roofline,
         "gossip_round": {"role": "gossip round alone (library-chosen gossip kernel + CSR/plan upload + finalize)",
                          "rp_updates_per_s": w.n * w.P / (gossip_ms * 1e-3),
                          "ms": round(gossip_ms, 4), "GBps": round(gossip_gbps, 1),
                          "frac_of_peak": round(gossip_gbps / PEAK_HBM_GBPS, 4), "bytes_per_rp": gossip_bytes,
-                         "traffic": read_traffic("gossip_round", w.name)},
+                         "traffic": read_traffic("gossip_round", wname)},
         "round_kernel": {"role": "fused_round" if args.fuse else "gossip_round",
                          "ms": round(float(np.mean(round_ms)), 4), "GBps": round(round_gbps, 1),
                          "frac_of_peak": round(round_gbps / PEAK_HBM_GBPS, 4),
@@ -313,7 +330,7 @@ def main():
     if not args.no_cpu_baseline:
         columns = min(args.cpu_columns, w.P) if args.cpu_columns > 0 else cpu_sample_columns(w, H_i)
         log("bench: timing the oracle on %d columns" % columns)
-        out["cpu_baseline"] = cpu_baseline(w, H_i, columns)
+        out["cpu_baseline"] = cpu_baseline(w, H_i, columns, args.form)
     print(json.dumps(out), flush=True)
 
 

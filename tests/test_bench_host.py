@@ -118,7 +118,9 @@ def test_cpu_baseline_times_the_oracle_on_a_sample(bench):
     out = bench.cpu_baseline(w, gi.local_steps(w), 2000)
     assert out["kind"] == "oracle" and out["cores"] == 1
     assert out["unit"] == "replica-param updates/s" and out["value"] > 0
-    assert "2000 of 350000000 columns x 16 workers" in out["sample"]
+    assert "2000 of 350000000 columns x 16 workers, one round (10 local steps + EQ round + CE)" in out["sample"]
+    alt = bench.cpu_baseline(w, gi.local_steps(w), 500, "local_dadam")
+    assert "local_dadam round" in alt["sample"] and alt["value"] > 0
 
 
 def test_cpu_sample_is_a_fixed_amount_of_work(bench):
@@ -133,3 +135,25 @@ def test_cpu_sample_is_a_fixed_amount_of_work(bench):
             assert abs(work - bench.CPU_SAMPLE_UNITS) <= w.n * (H_i.mean() + 1)
     assert sizes["onepeer-exp-n16-p350m"] == 30_000_000
     assert sizes["ring-n4-p1m"] == 1_048_576  # the whole row
+
+
+@pytest.mark.parametrize("sp", [4, 2])
+@pytest.mark.parametrize("stepped", [True, False])
+def test_round_form_bytes_are_the_buffers_they_stream(bench, sp, stepped):
+    # Algorithm 1: the slot holds y_j (x_j for a worker that did not step),
+    # each row reads x_i and u_i and writes x_i and u_i
+    assert bench.gossip_bytes_per_rp(sp, 0.0, stepped=stepped, form="alg1") == moved(
+        {"x": sp, "y or x": sp, "u": 4}, {"x": sp, "u": 4})
+    # DAdam (App. C): x_j in the slot, y_i for a worker that stepped, x written
+    dadam_reads = {"x": sp, "y": sp} if stepped else {"x": sp}
+    assert bench.gossip_bytes_per_rp(sp, 0.0, stepped=stepped, form="dadam") == moved(dadam_reads, {"x": sp})
+    # Local-DAdam: as DAdam plus the outer momentum u read and written
+    assert bench.gossip_bytes_per_rp(sp, 0.0, stepped=stepped, form="local_dadam") == moved(
+        dict(dadam_reads, u=4), {"x": sp, "u": 4})
+    # consensus momentum exists in EQ only
+    for form in ("alg1", "dadam", "local_dadam"):
+        assert bench.gossip_bytes_per_rp(sp, 0.1, stepped=stepped, form=form) == \
+            bench.gossip_bytes_per_rp(sp, 0.0, stepped=stepped, form=form)
+    # the fused last step adds g, m, v read and m, v written to an active worker
+    assert bench.fused_bytes_per_rp(sp, 0.0, True, stepped, form="alg1") == \
+        bench.gossip_bytes_per_rp(sp, 0.0, stepped=stepped, form="alg1") + 20
