@@ -382,7 +382,22 @@ class GASLoC:
         gasloc_replica_mean(self.ctx, out)
 
     def counters(self):
+        """(k, stepped, rounds_done): per-worker AdamW step counts, which workers
+        stepped since the last round, and the rounds done (for checkpoints)."""
         return gasloc_get_counters(self.ctx, self.n)
+
+    def set_counters(self, k, stepped, rounds_done):
+        """Restore the counters of a checkpoint (with the [n, ld] buffers)."""
+        gasloc_set_counters(self.ctx, k, stepped, rounds_done)
+
+    def set_alive(self, alive=None):
+        """Mark dead workers (uint8 [n], 0 = dead; None = all alive): they skip
+        their exchanges and local steps."""
+        gasloc_set_alive(self.ctx, alive)
+
+    def topology_csr(self, t):
+        """The generated mixing matrix of round t as (row_ptr, col, val)."""
+        return gasloc_topology_csr(self.ctx, t, self.n)
 
     def close(self):
         if self.__dict__.get("ctx"):

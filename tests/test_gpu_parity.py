@@ -231,7 +231,7 @@ def test_dead_workers_match_the_oracle_with_skipped_exchanges():
     # the library applies the mask itself; the oracle is given the masked W
     # and the masked local steps explicitly
     pair2 = Pair(n, P, "two_peer", "f32", gamma=0.1)
-    g.gasloc_set_alive(pair2.gpu.ctx, alive)
+    pair2.gpu.set_alive(alive)
     for t in range(3):
         gi.fill_grads(pair2.grads, pair2.mu_i, pair2.step)
         g_host = pair2.grads[:, pair2.cols_dev].cpu().numpy()
@@ -425,7 +425,7 @@ def test_checkpoint_resume_is_bit_exact():
     torch.cuda.synchronize()
     for name, t_ in saved.items():
         getattr(resumed.gpu, name).copy_(t_)
-    g.gasloc_set_counters(resumed.gpu.ctx, k, stepped, rounds)
+    resumed.gpu.set_counters(k, stepped, rounds)
     resumed.step = step
     for t in range(2, 4):
         resumed.local_step()
@@ -503,7 +503,7 @@ def test_topology_csr_from_context_matches_oracle():
 
     gpu = g.GASLoC(32, 256, topology="random_regular", seed=3, degree=3)
     for t in range(20):
-        got = g.gasloc_topology_csr(gpu.ctx, t, 32)
+        got = gpu.topology_csr(t)
         exp = oracle.topology_csr("random_regular", 32, 3, t, 3)
         for a, b in zip(got, exp):
             assert np.array_equal(a, b)
