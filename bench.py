@@ -25,7 +25,8 @@ METRIC = "replica-param updates/s per gossip round; achieved HBM GB/s vs peak"
 DEFAULT_WORKLOAD = "onepeer-exp-n16-p350m"
 # the kernels and the code that picks them and their launch shapes
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_11081_amd", "csrc", f)
-                  for f in ("kernels.hip", "runtime.cpp", "plan.cpp")]
+                  for f in ("device_common.h", "adamw.hip", "round_phase.hip", "round_planned.hip", "reductions.hip",
+                            "runtime.cpp", "plan.cpp")]
 
 
 def log(msg):

@@ -1,5 +1,7 @@
-// Internal interfaces between the C ABI (runtime.cpp), the schedule generator
-// (topology.cpp) and the HIP kernels (kernels.hip).  Not installed.
+// Internal interfaces between the C ABI (runtime.cpp), the schedule
+// generator (topology.cpp), the visit planner (plan.cpp) and the HIP kernels
+// (adamw.hip, round_phase.hip, round_planned.hip, reductions.hip, with the
+// device helpers of device_common.h).  Not installed.
 #pragma once
 
 #include <hip/hip_runtime_api.h>
@@ -110,9 +112,11 @@ hipError_t launch_gossip_round(const GossipArgs& a, int dtype, bool fused, int f
                                const LaunchShape& shape, hipStream_t stream);
 hipError_t launch_gossip_planned(const GossipArgs& a, int dtype, bool fused, int form, const LaunchShape& shape,
                                  hipStream_t stream);
-// Workgroups of the selected round kernel that one CU holds at once, given
-// its registers, LDS and wave limits (0 if the query fails).
-int round_blocks_per_cu(int dtype, bool fused, int form, bool planned, const LaunchShape& shape, size_t dyn_lds);
+// Workgroups of the selected phase or planned round kernel that one CU
+// holds at once, given its registers, LDS and wave limits (0 if the query
+// fails).
+int phase_blocks_per_cu(int dtype, bool fused, int form, const LaunchShape& shape, size_t dyn_lds);
+int planned_blocks_per_cu(int dtype, bool fused, int form, const LaunchShape& shape, size_t dyn_lds);
 // Dynamic LDS bytes of one workgroup of the planned kernel (z slots only).
 size_t planned_lds_bytes(int slots, const LaunchShape& shape);
 hipError_t launch_consensus_error(const void* x, int dtype, int64_t ld, int n, int64_t p_begin,

@@ -1,0 +1,182 @@
+// a5 standalone and a6: the consensus error of the stored x over a column
+// range, the fixed-order fp64 finalize of workgroup partials, and the
+// network average.
+#pragma clang fp contract(off)
+
+#include "device_common.h"
+
+namespace gasloc {
+namespace {
+
+// Columns [lo, hi) of the V-column group at idx (the others read as 0): a
+// vector load when the whole group is in range.
+template <int DT, int V>
+__device__ __forceinline__ void load_cols(const void* base, int64_t idx, int lo, int hi, float (&o)[V]) {
+  if (lo == 0 && hi == V) {
+    load_params<DT, V>(base, idx, V, o);
+    return;
+  }
+#pragma unroll
+  for (int c = 0; c < V; ++c) {
+    if (c >= lo && c < hi) {
+      if constexpr (DT == GASLOC_BF16)
+        o[c] = bf16_to_f32(static_cast<const uint16_t*>(base)[idx + c]);
+      else
+        o[c] = static_cast<const float*>(base)[idx + c];
+    } else {
+      o[c] = 0.0f;
+    }
+  }
+}
+
+// A thread takes a group of columns of every worker (4 fp32 or 8 bf16, i.e.
+// 16 bytes; groups are aligned so every row's vector loads are, and the
+// groups at the ends of the range are masked), with the loads of 8 workers
+// (fp32) or 4 (bf16, twice the columns; 8 left it register-bound) in
+// flight.  Per column the sums are those of the fused kernel: shifted by
+// worker 0's value, fp64, workers in order.
+template <int DT>
+__global__ __launch_bounds__(256) void k_consensus_error(const void* x, int64_t ld, int n,
+                                                         int64_t p_begin, int64_t p_end,
+                                                         double* partials) {
+  constexpr int V = DT == GASLOC_BF16 ? 8 : 4, R = DT == GASLOC_BF16 ? 4 : 8;
+  const double inv_n = 1.0 / static_cast<double>(n);
+  const int64_t base = p_begin - p_begin % V;
+  const int64_t groups = (p_end - base + V - 1) / V;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  double ce = 0.0;
+  for (int64_t gi = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; gi < groups; gi += stride) {
+    const int64_t p = base + gi * V;
+    const int lo = p < p_begin ? static_cast<int>(p_begin - p) : 0;
+    const int hi = p_end - p < V ? static_cast<int>(p_end - p) : V;
+    double shift[V], s[V], q[V];
+    {
+      float v[V];
+      load_cols<DT, V>(x, p, lo, hi, v);
+#pragma unroll
+      for (int c = 0; c < V; ++c) {
+        shift[c] = static_cast<double>(v[c]);
+        s[c] = 0.0;
+        q[c] = 0.0;
+      }
+    }
+    for (int i0 = 1; i0 < n; i0 += R) {
+      float v[R][V];
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (i0 + r >= n) break;
+        load_cols<DT, V>(x, static_cast<int64_t>(i0 + r) * ld + p, lo, hi, v[r]);
+      }
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (i0 + r >= n) break;
+#pragma unroll
+        for (int c = 0; c < V; ++c) {
+          const double d = static_cast<double>(v[r][c]) - shift[c];
+          s[c] += d;
+          q[c] += d * d;
+        }
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < V; ++c)
+      if (c >= lo && c < hi) ce += q[c] - s[c] * s[c] * inv_n;
+  }
+  const double total = block_sum(ce);
+  if (threadIdx.x == 0) partials[blockIdx.x] = total;
+}
+
+// Fixed-order sum of `count` partials into *out (one workgroup).
+__global__ __launch_bounds__(256) void k_finalize(const double* partials, int count, double* out) {
+  double v = 0.0;
+  for (int k = threadIdx.x; k < count; k += blockDim.x) v += partials[k];
+  const double total = block_sum(v);
+  if (threadIdx.x == 0) *out = total;
+}
+
+// The same for the two partial arrays of a round (consensus error, squared
+// pseudo-gradients) in one launch: out[0], out[1], each in k_finalize's order.
+__global__ __launch_bounds__(256) void k_finalize2(const double* a, const double* b, int count, double* out) {
+  double va = 0.0, vb = 0.0;
+  for (int k = threadIdx.x; k < count; k += blockDim.x) {
+    va += a[k];
+    vb += b[k];
+  }
+  double ta, tb;
+  block_sum2(va, vb, ta, tb);
+  if (threadIdx.x == 0) {
+    out[0] = ta;
+    out[1] = tb;
+  }
+}
+
+// a6: network average, fp64 sum in worker order, rounded to the param dtype;
+// 16 bytes of columns per thread, the loads of 8 workers in flight at a time.
+template <int DT>
+__global__ __launch_bounds__(256) void k_replica_mean(const void* x, int64_t ld, int n, int64_t P,
+                                                      void* out) {
+  constexpr int V = DT == GASLOC_BF16 ? 8 : 4, R = 8;
+  const int64_t groups = (P + V - 1) / V;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  for (int64_t gi = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; gi < groups; gi += stride) {
+    const int64_t p = gi * V;
+    const int cnt = static_cast<int>(P - p < V ? P - p : V);
+    double s[V];
+#pragma unroll
+    for (int c = 0; c < V; ++c) s[c] = 0.0;
+    for (int i0 = 0; i0 < n; i0 += R) {
+      float v[R][V];
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (i0 + r >= n) break;
+        load_params<DT, V>(x, static_cast<int64_t>(i0 + r) * ld + p, cnt, v[r]);
+      }
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (i0 + r >= n) break;
+#pragma unroll
+        for (int c = 0; c < V; ++c) s[c] += static_cast<double>(v[r][c]);
+      }
+    }
+    float mean[V], kept[V];
+#pragma unroll
+    for (int c = 0; c < V; ++c) mean[c] = static_cast<float>(s[c] / static_cast<double>(n));
+    store_params<DT, V>(out, p, cnt, mean, kept);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_consensus_error(const void* x, int dtype, int64_t ld, int n, int64_t p_begin,
+                                  int64_t p_end, double* partials, int blocks, hipStream_t stream) {
+  if (dtype == GASLOC_BF16)
+    hipLaunchKernelGGL((k_consensus_error<GASLOC_BF16>), dim3(blocks), dim3(256), 0, stream, x, ld, n,
+                       p_begin, p_end, partials);
+  else
+    hipLaunchKernelGGL((k_consensus_error<GASLOC_F32>), dim3(blocks), dim3(256), 0, stream, x, ld, n,
+                       p_begin, p_end, partials);
+  return hipGetLastError();
+}
+
+hipError_t launch_finalize(const double* partials, int count, double* out, hipStream_t stream) {
+  hipLaunchKernelGGL(k_finalize, dim3(1), dim3(256), 0, stream, partials, count, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_finalize2(const double* a, const double* b, int count, double* out, hipStream_t stream) {
+  hipLaunchKernelGGL(k_finalize2, dim3(1), dim3(256), 0, stream, a, b, count, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_replica_mean(const void* x, int dtype, int64_t ld, int n, int64_t P, void* out,
+                               int blocks, hipStream_t stream) {
+  if (dtype == GASLOC_BF16)
+    hipLaunchKernelGGL((k_replica_mean<GASLOC_BF16>), dim3(blocks), dim3(256), 0, stream, x, ld, n, P,
+                       out);
+  else
+    hipLaunchKernelGGL((k_replica_mean<GASLOC_F32>), dim3(blocks), dim3(256), 0, stream, x, ld, n, P,
+                       out);
+  return hipGetLastError();
+}
+
+}  // namespace gasloc

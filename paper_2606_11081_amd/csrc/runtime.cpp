@@ -216,7 +216,8 @@ int lds_blocks_per_cu(const gasloc_ctx& c, size_t dyn_lds) {
 int resident_blocks_per_cu(const gasloc_ctx& c, const gasloc::LaunchShape& s, bool fused, bool planned,
                            size_t dyn_lds) {
   const int by_lds = std::min(lds_blocks_per_cu(c, dyn_lds), 2048 / s.threads);
-  const int query = gasloc::round_blocks_per_cu(c.hp.param_dtype, fused, c.hp.round_form, planned, s, dyn_lds);
+  const int query = planned ? gasloc::planned_blocks_per_cu(c.hp.param_dtype, fused, c.hp.round_form, s, dyn_lds)
+                            : gasloc::phase_blocks_per_cu(c.hp.param_dtype, fused, c.hp.round_form, s, dyn_lds);
   return std::max(1, query <= 0 ? by_lds : std::min(query, by_lds));  // a failed query leaves the LDS bound
 }
 
