@@ -752,3 +752,23 @@ def test_row_padding_is_never_touched(n, topology, dtype, form):
     tail = mean[P:].view(torch.int16) if dtype == "bf16" else mean[P:].view(torch.int32)
     assert bool((tail == (canary16 if dtype == "bf16" else canary32)).all()), "mean: padding written"
     assert bool(torch.isfinite(x[:, :P].float()).all()) and bool(torch.isfinite(mean[:P].float()).all())
+
+
+@pytest.mark.parametrize("n,topology,dtype", [(16, "one_peer_exp", "f32"), (40, "two_peer", "bf16")])
+def test_long_run_stays_bit_identical(n, topology, dtype):
+    # 60 rounds (the phase kernel at n=16, the planned one at n=40), varying
+    # local-step counts and the fused last step every other round: the state
+    # never drifts from the fp32 oracle by a single bit
+    pair = Pair(n, 2_051, topology, dtype, gamma=0.2, precisions=("f32",))
+    rng = np.random.default_rng(77)
+    for t in range(60):
+        H = rng.integers(1, 4, n)
+        for h in range(int(H.max()) - 1):
+            pair.local_step(active=(H > h).astype(np.uint8))
+        if t % 2:
+            pair.local_step_gossip_round(t, active=(H == H.max()).astype(np.uint8))
+        else:
+            pair.local_step(active=(H == H.max()).astype(np.uint8))
+            pair.gossip_round(t)
+    reduction_close(pair.gpu.consensus_error(), pair.oracles["f32"].consensus_error(), "CE after 60 rounds")
+    pair.check_state(tag="60 rounds")
