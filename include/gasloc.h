@@ -20,7 +20,10 @@
  *   - All device work is enqueued on the stream given to gasloc_init.  Only
  *     gasloc_consensus_error, gasloc_consensus_error_cols,
  *     gasloc_pseudo_gradient_sq and gasloc_destroy wait for the stream;
- *     kernel faults surface at the next blocking call.
+ *     kernel faults surface at the next blocking call.  A round that changes
+ *     the CSR (or visit plan) stages it in a ring of four pinned host
+ *     buffers, so it may wait for the upload of a round enqueued four
+ *     uploads earlier, never for kernels.
  *   - A context is not thread-safe; distinct contexts are independent.
  *   - After a device error every call on the context returns GASLOC_ESTATE.
  */
