@@ -22,8 +22,8 @@
  *     gasloc_pseudo_gradient_sq and gasloc_destroy wait for the stream;
  *     kernel faults surface at the next blocking call.  A round that changes
  *     the CSR (or visit plan) stages it in a ring of four pinned host
- *     buffers, so it may wait for the upload of a round enqueued four
- *     uploads earlier, never for kernels.
+ *     buffers, so it may wait until the stream has passed the upload made
+ *     four uploads earlier (with all work enqueued before that upload).
  *   - A context is not thread-safe; distinct contexts are independent.
  *   - After a device error every call on the context returns GASLOC_ESTATE.
  */
