@@ -369,6 +369,74 @@ def test_explicit_csr_with_equal_rows(form, dtype):
     pair.check_state(tag="equal rows %s %s" % (form, dtype))
 
 
+def _bf16_edge_pairs(rng, P):
+    """Two rows of bf16 bit patterns whose fp32 midpoints meet the rounding
+    cases: adjacent values (exact ties, both parities of the lower one), random
+    finite values, subnormals, signed zeros and the largest finite values."""
+    finite = lambda k: rng.integers(0, 0x7F80, k).astype(np.uint16) | (rng.integers(0, 2, k).astype(np.uint16) << 15)
+    a = finite(P)
+    b = finite(P)
+    q = P // 5
+    b[:q] = a[:q] + 1  # the next bf16 value of the same sign: the midpoint is a tie
+    fix = (a[:q] & 0x7FFF) == 0x7F7F  # the next one after the largest finite is infinity
+    b[:q][fix] = a[:q][fix] - 1
+    sub = slice(q, 2 * q)  # subnormals (exponent field 0), either sign
+    a[sub] = (a[sub] & 0x807F)
+    b[sub] = (b[sub] & 0x807F)
+    z = 2 * q
+    a[z:z + 4] = [0x0000, 0x8000, 0x0000, 0x8000]  # +0, -0 in every combination
+    b[z:z + 4] = [0x0000, 0x0000, 0x8000, 0x8000]
+    a[z + 4:z + 8] = [0x7F7F, 0xFF7F, 0x7F7F, 0x7F7E]  # the largest finite values
+    b[z + 4:z + 8] = [0x7F7F, 0xFF7F, 0x7F7E, 0x7F7F]
+    return a, b
+
+
+@pytest.mark.parametrize("n", [2, 18])
+def test_bf16_rounding_edge_cases(n):
+    """bf16 stores round to nearest, ties to even, keep subnormals and signed
+    zeros, as the oracle does and as an independent rounding (torch's CPU
+    conversion) of the same fp32 sums does.  With no local steps, mu = gamma =
+    0 and rows averaging pairs of workers with weights 1/2, each stored value
+    is the rounding of (0 + z_a/2) + z_b/2, with z = x: the exact midpoint of
+    two stored values.  n = 2 runs the phase kernel, n = 18 the planned one."""
+    import torch
+
+    import paper_2606_11081_amd as g
+
+    P = 4099
+    rng = np.random.default_rng(21 + n)
+    bits = np.empty((n, P), np.uint16)
+    for k in range(0, n, 2):
+        bits[k], bits[k + 1] = _bf16_edge_pairs(rng, P)
+    log("case bf16 rounding: n=%d P=%d" % (n, P))
+    gpu = g.GASLoC(n, P, topology="ring", param_dtype="bf16", outer_momentum=0.0, consensus_momentum=0.0,
+                   outer_lr=0.7)
+    gpu.x[:, :P].view(torch.int16).copy_(torch.from_numpy(bits.view(np.int16)).cuda())
+    hp = oracle.OracleHParams(beta1=gi.BETA1, beta2=gi.BETA2, eps=gi.EPS, weight_decay=gi.WEIGHT_DECAY,
+                              outer_lr=0.7, outer_momentum=0.0, nesterov=True, consensus_momentum=0.0)
+    o = oracle.Oracle(n, P, hp, param_dtype="bf16")
+    o.x[...] = bits
+    o.y[...] = bits  # no local steps: y is x
+    W = _csr_from_rows([((k - k % 2, k - k % 2 + 1), (0.5, 0.5)) for k in range(n)])
+    gpu.gossip_round(0, W)
+    o.gossip_round(0, csr=W)
+    torch.cuda.synchronize()
+    got = gpu.x[:, :P].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    assert np.array_equal(got, o.x), "bf16 stores differ from the oracle"
+    # independent of both: fp32 sums in the same order, rounded by torch on the CPU
+    f = oracle.bf16_bits_to_f32(bits)
+    half = np.float32(0.5)
+    ref = np.empty_like(bits)
+    for k in range(n):
+        lo = k - k % 2
+        mid = (np.float32(0.0) + half * f[lo]) + half * f[lo + 1]
+        ref[k] = torch.from_numpy(mid).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(got, ref), "bf16 stores differ from round-to-nearest-even"
+    # the first fifth of each pair of rows are neighbours: every midpoint is a tie
+    assert np.all(got[:, : P // 5] % 2 == 0), "a tie did not go to the even neighbour"
+    gpu.close()
+
+
 def test_all_inactive_step_changes_nothing():
     import torch
 
