@@ -10,9 +10,12 @@
 // cache (constant address space): worker and slot indices, counts and weights
 // are wave-uniform and all control flow is scalar.  The loads of the next
 // super-step (of this column group, or the first of the next group) are issued
-// before the current one is computed, so a wave keeps one super-step of
-// operands in flight while it works; they are held as raw words and decoded at
-// their use, which keeps the loads outstanding until then.
+// before the current one is computed, so the loads of two super-steps are in
+// flight together; they are held as raw words and decoded at their use.
+// (Super-steps skip the loads they do not need, so the compiler's wait before
+// a computation also covers the next super-step's loads; a variant with the
+// same accesses on every path, whose waits left them in flight, measured no
+// faster.)
 //
 // Plan words: [S, start_0 .. start_{S-1}], super-step at start_s:
 //   npre, nrows, (worker, slot) x npre, row x nrows,
