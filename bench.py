@@ -92,10 +92,9 @@ def read_traffic(kernel, workload):
     return float(m.group(1))
 
 
-def cpu_baseline(w, H_i, columns, form="eq"):
-    """The oracle as it stands, single-threaded, on `columns` columns of the
-    same workload: one full round (all local steps, gossip, consensus error)
-    in the same round form."""
+def _oracle_sample(w, columns, form, seed):
+    """An oracle on `columns` columns of the workload, with its x0 and one
+    gradient batch (host arrays, made before any timing)."""
     import numpy as np
 
     import gasloc_inputs as gi
@@ -106,21 +105,90 @@ def cpu_baseline(w, H_i, columns, form="eq"):
                               nesterov=True, consensus_momentum=w.gamma if form == "eq" else 0.0, form=form)
     o = oracle.Oracle(w.n, columns, hp, topology=w.topology, seed=gi.SEED_TOPOLOGY, degree=w.degree,
                       precision="f32", param_dtype=w.param_dtype)
-    rng = np.random.default_rng(0)
-    x0 = (rng.standard_normal(columns) * 0.02).astype(np.float32)
-    o.set_params(x0)
+    rng = np.random.default_rng(seed)
+    o.set_params((rng.standard_normal(columns) * 0.02).astype(np.float32))
     g = (rng.standard_normal((w.n, columns)) + gi.worker_means(w.n)[:, None]).astype(np.float32)
-    t0 = time.perf_counter()
+    return o, g
+
+
+def _oracle_round(o, g, H_i):
+    """One full round on the oracle: every local step, the round, the
+    consensus error."""
+    import numpy as np
+
+    import gasloc_inputs as gi
+
     for h in range(int(H_i.max())):
         o.local_step(g, gi.LOCAL_LR, (H_i > h).astype(np.uint8))
     o.gossip_round(0)
     o.consensus_error()
+
+
+def cpu_baseline(w, H_i, columns, form="eq"):
+    """The oracle as it stands, single-threaded, on `columns` columns of the
+    same workload: one full round (all local steps, gossip, consensus error)
+    in the same round form."""
+    o, g = _oracle_sample(w, columns, form, 0)
+    t0 = time.perf_counter()
+    _oracle_round(o, g, H_i)
     dt = time.perf_counter() - t0
     return {"value": w.n * columns / dt, "unit": "replica-param updates/s", "cores": 1, "kind": "oracle",
             "sample": "%d of %d columns x %d workers, one round (%d local steps + %s round + CE), "
                       "plain C oracle (fp32 build, -O2, single thread on %s, %d host threads visible): %.2f s"
                       % (columns, w.P, w.n, int(H_i.max()), form.upper() if form == "eq" else form, host_cpu(),
                          os.cpu_count() or 0, dt)}
+
+
+def host_threads():
+    """Host threads this process may use: its CPU affinity, capped by
+    OMP_NUM_THREADS when that is set."""
+    try:
+        t = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        t = os.cpu_count() or 1
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        t = min(t, int(env))
+    return max(1, t)
+
+
+def cpu_baseline_parallel(w, H_i, columns, form="eq", threads=None):
+    """The same oracle on all host threads: the sample's columns split into
+    one contiguous slice per thread, each slice an oracle of its own (every
+    stored value depends only on its own column, so the slices are
+    independent), run concurrently.  The oracle's C calls release the GIL."""
+    import threading
+
+    threads = threads or host_threads()
+    threads = max(1, min(threads, columns))
+    bounds = [columns * k // threads for k in range(threads + 1)]
+    parts = [_oracle_sample(w, bounds[k + 1] - bounds[k], form, 100 + k) for k in range(threads)]
+    start = threading.Barrier(threads + 1)
+    errors = []
+
+    def run(k):
+        start.wait()
+        try:
+            _oracle_round(parts[k][0], parts[k][1], H_i)
+        except Exception as e:  # reported after the join
+            errors.append(e)
+
+    pool = [threading.Thread(target=run, args=(k,)) for k in range(threads)]
+    for t in pool:
+        t.start()
+    start.wait()
+    t0 = time.perf_counter()
+    for t in pool:
+        t.join()
+    dt = time.perf_counter() - t0
+    if errors:
+        raise errors[0]
+    return {"value": w.n * columns / dt, "unit": "replica-param updates/s", "cores": threads, "kind": "oracle",
+            "sample": "%d of %d columns x %d workers, one round (%d local steps + %s round + CE), "
+                      "plain C oracle (fp32 build, -O2) on %d threads of %s, one contiguous column slice "
+                      "per thread: %.2f s"
+                      % (columns, w.P, w.n, int(H_i.max()), form.upper() if form == "eq" else form, threads,
+                         host_cpu(), dt)}
 
 
 # Oracle work units (one worker-column through one local step or one gossip
@@ -332,6 +400,8 @@ def main():
         columns = min(args.cpu_columns, w.P) if args.cpu_columns > 0 else cpu_sample_columns(w, H_i)
         log("bench: timing the oracle on %d columns" % columns)
         out["cpu_baseline"] = cpu_baseline(w, H_i, columns, args.form)
+        log("bench: timing the oracle on %d host threads" % host_threads())
+        out["cpu_baseline_all_threads"] = cpu_baseline_parallel(w, H_i, columns, args.form)
     print(json.dumps(out), flush=True)
 
 

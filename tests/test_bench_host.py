@@ -7,6 +7,7 @@ import re
 import subprocess
 import sys
 
+import numpy as np
 import pytest
 
 import gasloc_inputs as gi
@@ -121,6 +122,40 @@ def test_cpu_baseline_times_the_oracle_on_a_sample(bench):
     assert "2000 of 350000000 columns x 16 workers, one round (10 local steps + EQ round + CE)" in out["sample"]
     alt = bench.cpu_baseline(w, gi.local_steps(w), 500, "local_dadam")
     assert "local_dadam round" in alt["sample"] and alt["value"] > 0
+
+
+def test_cpu_baseline_on_all_threads_splits_the_sample(bench):
+    w = gi.WORKLOADS[bench.DEFAULT_WORKLOAD]
+    out = bench.cpu_baseline_parallel(w, gi.local_steps(w), 2001, threads=3)
+    assert out["kind"] == "oracle" and out["cores"] == 3
+    assert out["unit"] == "replica-param updates/s" and out["value"] > 0
+    assert "2001 of 350000000 columns x 16 workers" in out["sample"] and "on 3 threads" in out["sample"]
+    assert bench.cpu_baseline_parallel(w, gi.local_steps(w), 2, threads=8)["cores"] == 2
+    assert bench.host_threads() >= 1
+
+
+def test_oracle_column_slices_are_independent(bench):
+    """The all-threads baseline runs the oracle on column slices; a round on
+    each slice gives exactly the columns of a round on the whole row."""
+    import oracle
+
+    w = gi.WORKLOADS["regular3-n32-p150m-bf16"]
+    H_i = np.array([1 + (i % 3) for i in range(w.n)])
+    P = 3001
+    full, g = bench._oracle_sample(w, P, "eq", 7)
+    x0 = full.x[0].copy()
+    bench._oracle_round(full, g, H_i)
+    bench._oracle_round(full, g, H_i)  # the second round applies the consensus momentum
+    cuts = [0, 1000, 1001, P]
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        part, _ = bench._oracle_sample(w, b - a, "eq", 7)
+        part.set_params(x0[a:b])
+        gs = np.ascontiguousarray(g[:, a:b])
+        bench._oracle_round(part, gs, H_i)
+        bench._oracle_round(part, gs, H_i)
+        for name in ("x", "y", "m", "v", "u", "zp"):
+            assert np.array_equal(getattr(part, name), getattr(full, name)[:, a:b]), name
+    assert isinstance(full, oracle.Oracle)
 
 
 def test_cpu_sample_is_a_fixed_amount_of_work(bench):
