@@ -24,19 +24,32 @@ PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, AMD specification
 METRIC = "replica-param updates/s per gossip round; achieved HBM GB/s vs peak"
 DEFAULT_WORKLOAD = "onepeer-exp-n16-p350m"
 # the kernels and the code that picks them and their launch shapes
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_11081_amd", "csrc", f)
-                  for f in ("device_common.h", "adamw.hip", "round_phase.hip", "round_planned.hip", "reductions.hip",
-                            "runtime.cpp", "plan.cpp")]
+CSRC = os.path.join(ROOT, "paper_2606_11081_amd", "csrc")
+# the sources each kernel family is compiled and launched from: a committed
+# counter summary stays valid while its family's sources are unchanged
+KERNEL_FAMILIES = {
+    "adamw": ("device_common.h", "internal.h", "adamw.hip", "runtime.cpp"),
+    "phase": ("device_common.h", "internal.h", "round_phase.hip", "reductions.hip", "runtime.cpp"),
+    "planned": ("device_common.h", "internal.h", "round_planned.hip", "reductions.hip", "runtime.cpp", "plan.cpp"),
+}
 
 
-def log(msg):
-    print(msg, file=sys.stderr, flush=True)
+def kernel_family(kernel, n):
+    """Family of the kernel behind a profiled role: AdamW, or the gossip
+    kernel the library picks for n workers (the planned kernel beyond 16,
+    unless GASLOC_GOSSIP_KERNEL forces one)."""
+    if kernel == "k_local_adamw":
+        return "adamw"
+    forced = os.environ.get("GASLOC_GOSSIP_KERNEL", "")
+    if forced in ("phase", "planned"):
+        return forced
+    return "planned" if n > 16 else "phase"
 
 
-def kernels_sha():
+def kernels_sha(family):
     h = hashlib.sha256()
-    for path in KERNEL_SOURCES:
-        with open(path, "rb") as f:
+    for name in KERNEL_FAMILIES[family]:
+        with open(os.path.join(CSRC, name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
@@ -79,15 +92,15 @@ def fused_bytes_per_rp(sp, gamma, active, stepped, with_u=True, form="eq"):
     return b
 
 
-def read_traffic(kernel, workload):
+def read_traffic(kernel, workload, n):
     """HBM bytes per dispatch from a committed rocprofv3 --pmc summary, or None
-    if absent or taken on a different kernel source."""
+    if absent or taken on other sources of the kernel's family."""
     path = os.path.join(ROOT, "profiles", "%s_%s_pmc.md" % (kernel, workload))  # kernel: a kernel or role name
     if not os.path.exists(path):
         return None
     text = open(path).read()
     m = re.search(r"traffic_bytes_per_dispatch:\s*([0-9.eE+]+)\s+kernels_sha:\s*([0-9a-f]+)", text)
-    if not m or m.group(2) != kernels_sha():
+    if not m or m.group(2) != kernels_sha(kernel_family(kernel, n)):
         return None
     return float(m.group(1))
 
@@ -360,7 +373,7 @@ def main():
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
-                "traffic": read_traffic(dom, wname),
+                "traffic": read_traffic(dom, wname, w.n),
                 "algorithmic_bytes_per_launch": int(dom_bytes), "avg_launch_ms": round(dom_ms, 4)}
     out = {
         "metric": METRIC,
@@ -382,7 +395,7 @@ def main():
                          "rp_updates_per_s": w.n * w.P / (gossip_ms * 1e-3),
                          "ms": round(gossip_ms, 4), "GBps": round(gossip_gbps, 1),
                          "frac_of_peak": round(gossip_gbps / PEAK_HBM_GBPS, 4), "bytes_per_rp": gossip_bytes,
-                         "traffic": read_traffic("gossip_round", wname)},
+                         "traffic": read_traffic("gossip_round", wname, w.n)},
         "round_kernel": {"role": "fused_round" if args.fuse else "gossip_round",
                          "ms": round(float(np.mean(round_ms)), 4), "GBps": round(round_gbps, 1),
                          "frac_of_peak": round(round_gbps / PEAK_HBM_GBPS, 4),

@@ -291,21 +291,39 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
     float acc[V];
 #pragma unroll
     for (int c = 0; c < V; ++c) acc[c] = reuse ? cs.mix[c] : 0.0f;
-    for (int k0 = 0; k0 < count; k0 += 4) {
+    // rows of exactly four entries (every row of a 3-regular graph with its
+    // self-loop) take a branch-free path; the summation order is the same
+    if (count == 4) {
       float zk[4][V], wk[4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        if (k0 + t >= count) break;
-        const float* src = mine + ops[pos + 2 + 2 * (k0 + t)] * slot_stride;
-        wk[t] = __int_as_float(ops[pos + 3 + 2 * (k0 + t)]);
+        const float* src = mine + ops[pos + 2 + 2 * t] * slot_stride;
+        wk[t] = __int_as_float(ops[pos + 3 + 2 * t]);
 #pragma unroll
         for (int c = 0; c < V; ++c) zk[t][c] = src[c];
       }
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        if (k0 + t >= count) break;
 #pragma unroll
         for (int c = 0; c < V; ++c) acc[c] = acc[c] + wk[t] * (kDiff ? xi[c] - zk[t][c] : zk[t][c]);
+      }
+    } else {
+      for (int k0 = 0; k0 < count; k0 += 4) {
+        float zk[4][V], wk[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          if (k0 + t >= count) break;
+          const float* src = mine + ops[pos + 2 + 2 * (k0 + t)] * slot_stride;
+          wk[t] = __int_as_float(ops[pos + 3 + 2 * (k0 + t)]);
+#pragma unroll
+          for (int c = 0; c < V; ++c) zk[t][c] = src[c];
+        }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          if (k0 + t >= count) break;
+#pragma unroll
+          for (int c = 0; c < V; ++c) acc[c] = acc[c] + wk[t] * (kDiff ? xi[c] - zk[t][c] : zk[t][c]);
+        }
       }
     }
     pos += 2 + 2 * count;

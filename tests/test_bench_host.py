@@ -107,11 +107,32 @@ def test_traffic_is_withheld_for_another_kernel_source(bench, tmp_path, monkeypa
     prof.mkdir()
     (prof / "k_local_adamw_w_pmc.md").write_text("traffic_bytes_per_dispatch: 1.5e+11 kernels_sha: 0123456789abcdef\n")
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
-    monkeypatch.setattr(bench, "kernels_sha", lambda: "0123456789abcdef")
-    assert bench.read_traffic("k_local_adamw", "w") == 1.5e11
-    monkeypatch.setattr(bench, "kernels_sha", lambda: "fedcba9876543210")
-    assert bench.read_traffic("k_local_adamw", "w") is None
-    assert bench.read_traffic("missing", "w") is None
+    monkeypatch.setattr(bench, "kernels_sha", lambda family: "0123456789abcdef")
+    assert bench.read_traffic("k_local_adamw", "w", 16) == 1.5e11
+    monkeypatch.setattr(bench, "kernels_sha", lambda family: "fedcba9876543210")
+    assert bench.read_traffic("k_local_adamw", "w", 16) is None
+    assert bench.read_traffic("missing", "w", 16) is None
+
+
+def test_kernel_families_hash_their_own_sources(bench, tmp_path, monkeypatch):
+    import shutil
+
+    monkeypatch.delenv("GASLOC_GOSSIP_KERNEL", raising=False)
+    assert bench.kernel_family("k_local_adamw", 64) == "adamw"
+    assert bench.kernel_family("gossip_round", 16) == "phase"
+    assert bench.kernel_family("fused_round", 17) == "planned"
+    monkeypatch.setenv("GASLOC_GOSSIP_KERNEL", "planned")
+    assert bench.kernel_family("gossip_round", 8) == "planned"
+    names = sorted({f for files in bench.KERNEL_FAMILIES.values() for f in files})
+    for f in names:
+        shutil.copy(os.path.join(bench.CSRC, f), tmp_path / f)
+    monkeypatch.setattr(bench, "CSRC", str(tmp_path))
+    before = {fam: bench.kernels_sha(fam) for fam in bench.KERNEL_FAMILIES}
+    with open(tmp_path / "round_planned.hip", "a") as fh:
+        fh.write("// edited\n")
+    after = {fam: bench.kernels_sha(fam) for fam in bench.KERNEL_FAMILIES}
+    assert after["planned"] != before["planned"]
+    assert after["adamw"] == before["adamw"] and after["phase"] == before["phase"]
 
 
 def test_cpu_baseline_times_the_oracle_on_a_sample(bench):
