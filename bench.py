@@ -23,7 +23,12 @@ sys.path.insert(0, ROOT)
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, AMD specification
 METRIC = "replica-param updates/s per gossip round; achieved HBM GB/s vs peak"
 DEFAULT_WORKLOAD = "onepeer-exp-n16-p350m"
-# the kernels and the code that picks them and their launch shapes
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
 CSRC = os.path.join(ROOT, "paper_2606_11081_amd", "csrc")
 # the sources each kernel family is compiled and launched from: a committed
 # counter summary stays valid while its family's sources are unchanged

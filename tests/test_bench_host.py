@@ -213,3 +213,28 @@ def test_round_form_bytes_are_the_buffers_they_stream(bench, sp, stepped):
     # the fused last step adds g, m, v read and m, v written to an active worker
     assert bench.fused_bytes_per_rp(sp, 0.0, True, stepped, form="alg1") == \
         bench.gossip_bytes_per_rp(sp, 0.0, stepped=stepped, form="alg1") + 20
+
+
+def test_scripts_use_no_unbound_names():
+    """Every name the benchmark and the entry points read is bound somewhere
+    in the file or is a builtin (main() itself needs a GPU to run)."""
+    import ast
+    import builtins
+
+    for script in ("bench.py", "__graft_entry__.py"):
+        tree = ast.parse(open(os.path.join(ROOT, script)).read())
+        bound = set(dir(builtins)) | {"__file__", "__name__"}
+        for node in ast.walk(tree):
+            if isinstance(node, (ast.FunctionDef, ast.AsyncFunctionDef, ast.ClassDef)):
+                bound.add(node.name)
+            elif isinstance(node, ast.arg):
+                bound.add(node.arg)
+            elif isinstance(node, ast.Name) and isinstance(node.ctx, (ast.Store, ast.Del)):
+                bound.add(node.id)
+            elif isinstance(node, (ast.Import, ast.ImportFrom)):
+                bound.update((a.asname or a.name).split(".")[0] for a in node.names)
+            elif isinstance(node, ast.ExceptHandler) and node.name:
+                bound.add(node.name)
+        unbound = sorted({n.id for n in ast.walk(tree) if isinstance(n, ast.Name) and isinstance(n.ctx, ast.Load)}
+                         - bound)
+        assert not unbound, (script, unbound)
