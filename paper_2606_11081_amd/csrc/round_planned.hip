@@ -292,8 +292,11 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
 #pragma unroll
     for (int c = 0; c < V; ++c) acc[c] = reuse ? cs.mix[c] : 0.0f;
     // rows of exactly four entries (every row of a 3-regular graph with its
-    // self-loop) take a branch-free path; the summation order is the same
-    if (count == 4) {
+    // self-loop) take a branch-free path; the summation order is the same.
+    // Only in the EQ form at 2 columns per thread (the many-slot plans such
+    // graphs need): elsewhere the extra path costs registers and occupancy
+    constexpr bool kFour = kEq && V == 2;
+    if (kFour && count == 4) {
       float zk[4][V], wk[4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
