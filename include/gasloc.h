@@ -26,6 +26,11 @@
  *     four uploads earlier (with all work enqueued before that upload).
  *   - A context is not thread-safe; distinct contexts are independent.
  *   - After a device error every call on the context returns GASLOC_ESTATE.
+ *   - The library reads one environment variable, a test hook:
+ *     GASLOC_GOSSIP_KERNEL=phase|planned forces the round kernel (by default
+ *     the kernel that keeps every worker's value in LDS runs for n <= 16, the
+ *     host-planned slot-reusing kernel beyond); results are bit-identical
+ *     either way.
  */
 #ifndef GASLOC_H
 #define GASLOC_H
@@ -160,7 +165,8 @@ typedef struct gasloc_ctx gasloc_ctx;
  * x_{t,0} = x_t in Eq. 1).  The buffers must outlive the context.
  * Errors: EINVAL for n, P, ld, alignment, NULL buffers, hyperparameters out
  * of range, bad topology (EXPLICIT is allowed: pass W to every round);
- * ENOMEM; EDEVICE. */
+ * ENOMEM when a host or device allocation runs out of memory; EDEVICE for
+ * any other HIP failure. */
 gasloc_status gasloc_init(int32_t n, int64_t P, const gasloc_topology *topology,
                           const gasloc_hparams *hparams, const gasloc_buffers *buffers,
                           void *hip_stream, gasloc_ctx **out);

@@ -16,6 +16,10 @@ namespace gasloc {
 
 constexpr int kMaxReplicas = 64;
 
+// Message of the last failing context-free call on this thread (what
+// gasloc_last_error(NULL) returns).
+void set_thread_error(const std::string& msg);
+
 bool make_topology(const gasloc_topology& topo, int n, uint64_t t, int32_t* row_ptr, int32_t* col,
                    float* val, int32_t cap, int32_t* nnz, std::string* err);
 // Visit plan of a round for the slot-reusing kernel (plan.cpp): super-steps
@@ -61,7 +65,9 @@ struct AdamArgs {
 
 // One gossip round; the consensus-error partial of every workgroup goes to
 // partials[blockIdx.x], its partial sum of squared pseudo-gradients to
-// pg_partials[blockIdx.x].
+// pg_partials[blockIdx.x].  Workgroup b takes the column groups [b * tile_groups,
+// (b + 1) * tile_groups) (a multiple of the workgroup size), in steps of one
+// group per thread.
 struct GossipArgs {
   void* x;
   const void* y;
@@ -73,6 +79,7 @@ struct GossipArgs {
   double* partials;
   double* pg_partials;
   int64_t ld, P;
+  int64_t tile_groups;
   int32_t n, nnz;
   float mu, eta, gamma;
   int32_t nesterov;
@@ -100,14 +107,15 @@ struct GossipArgs {
 };
 
 struct LaunchShape {
-  int vec;      // columns per thread per iteration (1, 2 or 4)
+  int vec;      // columns per thread per step (1, 2 or 4)
   int threads;  // workgroup size
-  int blocks;   // workgroups (grid-stride loop inside)
+  int blocks;   // workgroups: one per tile of `per` steps of the workgroup
   int batch;    // workers whose loads are issued together (1, 2, 4 or 8)
+  int per;      // steps (threads * vec columns each) per workgroup
 };
 
 // Launchers: enqueue on `stream`, return the launch status.
-hipError_t launch_local_adamw(const AdamArgs& a, int dtype, int blocks_per_worker, hipStream_t stream);
+hipError_t launch_local_adamw(const AdamArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_gossip_round(const GossipArgs& a, int dtype, bool fused, int form,
                                const LaunchShape& shape, hipStream_t stream);
 hipError_t launch_gossip_planned(const GossipArgs& a, int dtype, bool fused, int form, const LaunchShape& shape,
@@ -124,6 +132,14 @@ hipError_t launch_consensus_error(const void* x, int dtype, int64_t ld, int n, i
 hipError_t launch_finalize(const double* partials, int count, double* out, hipStream_t stream);
 // out[0] = sum of a[0..count), out[1] = sum of b[0..count), each as launch_finalize sums.
 hipError_t launch_finalize2(const double* a, const double* b, int count, double* out, hipStream_t stream);
+// The same sums for up to kMaxPartials partials per array, in a fixed order
+// that depends only on count: beyond kFinalizeSegment partials, segments of
+// kFinalizeSegment consecutive partials are summed first (into seg[0..S) and
+// seg[S..2S), S = ceil(count / kFinalizeSegment)), then the segment sums.
+constexpr int kFinalizeSegment = 4096;
+constexpr int kMaxPartials = 1 << 20;
+hipError_t launch_finalize2_large(const double* a, const double* b, int count, double* seg, double* out,
+                                  hipStream_t stream);
 hipError_t launch_replica_mean(const void* x, int dtype, int64_t ld, int n, int64_t P, void* out,
                                int blocks, hipStream_t stream);
 

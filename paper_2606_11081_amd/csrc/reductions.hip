@@ -110,6 +110,26 @@ __global__ __launch_bounds__(256) void k_finalize2(const double* a, const double
   }
 }
 
+// First level of launch_finalize2_large: workgroup s sums the partials
+// [s * kFinalizeSegment, (s + 1) * kFinalizeSegment) of both arrays (fewer in
+// the last segment) in k_finalize2's order, into seg[s] and seg[S + s].
+__global__ __launch_bounds__(256) void k_finalize_segments(const double* a, const double* b, int count,
+                                                           double* seg) {
+  const int begin = blockIdx.x * kFinalizeSegment;
+  const int end = count - begin < kFinalizeSegment ? count : begin + kFinalizeSegment;
+  double va = 0.0, vb = 0.0;
+  for (int k = begin + threadIdx.x; k < end; k += blockDim.x) {
+    va += a[k];
+    vb += b[k];
+  }
+  double ta, tb;
+  block_sum2(va, vb, ta, tb);
+  if (threadIdx.x == 0) {
+    seg[blockIdx.x] = ta;
+    seg[gridDim.x + blockIdx.x] = tb;
+  }
+}
+
 // a6: network average, fp64 sum in worker order, rounded to the param dtype;
 // 16 bytes of columns per thread, the loads of 8 workers in flight at a time.
 template <int DT>
@@ -166,6 +186,16 @@ hipError_t launch_finalize(const double* partials, int count, double* out, hipSt
 hipError_t launch_finalize2(const double* a, const double* b, int count, double* out, hipStream_t stream) {
   hipLaunchKernelGGL(k_finalize2, dim3(1), dim3(256), 0, stream, a, b, count, out);
   return hipGetLastError();
+}
+
+hipError_t launch_finalize2_large(const double* a, const double* b, int count, double* seg, double* out,
+                                  hipStream_t stream) {
+  if (count <= kFinalizeSegment) return launch_finalize2(a, b, count, out, stream);
+  const int segments = (count + kFinalizeSegment - 1) / kFinalizeSegment;
+  hipLaunchKernelGGL(k_finalize_segments, dim3(segments), dim3(256), 0, stream, a, b, count, seg);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_finalize2(seg, seg + segments, segments, out, stream);
 }
 
 hipError_t launch_replica_mean(const void* x, int dtype, int64_t ld, int n, int64_t P, void* out,

@@ -50,9 +50,10 @@ __global__ __launch_bounds__(256) void k_gossip_round(GossipArgs a) {
   constexpr bool kMixesX = FORM == GASLOC_FORM_DADAM || FORM == GASLOC_FORM_LOCAL_DADAM;
   const double inv_n = 1.0 / static_cast<double>(n);
   const int64_t groups = (a.P + V - 1) / V;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * nt;
+  const int64_t g_begin = static_cast<int64_t>(blockIdx.x) * a.tile_groups;
+  const int64_t g_end = groups - g_begin < a.tile_groups ? groups : g_begin + a.tile_groups;
   double ce = 0.0, pg = 0.0;  // consensus error, squared pseudo-gradients
-  for (int64_t gi = static_cast<int64_t>(blockIdx.x) * nt + tid; gi < groups; gi += stride) {
+  for (int64_t gi = g_begin + tid; gi < g_end; gi += nt) {
     const int64_t p = gi * V;
     const int cnt = static_cast<int>(a.P - p < V ? a.P - p : V);
     auto slot = [&](int j) { return zs + (static_cast<size_t>(j) * nt + tid) * V; };

@@ -410,18 +410,21 @@ __global__ __launch_bounds__(256) void k_gossip_planned(GossipArgs a) {
   const int slot_stride = nt * V;
   float* mine = zs + tid * V;
 
-  // column groups blockIdx.x * nt + it * (gridDim.x * nt) + tid, it < iters:
-  // the same count for every thread of the workgroup, so control stays
-  // uniform.  Every iteration but possibly the last gives each thread V
-  // columns; in that last one threads past P see cnt < V (0 beyond the end)
+  // column groups (t0 + it) * nt + tid for the workgroup's steps it < iters
+  // (steps t0 .. t0 + iters - 1 of nt groups each): the same count for every
+  // thread of the workgroup, so control stays uniform.  Every step but the
+  // last one of the whole row gives each thread V columns; in that one,
+  // threads past P see cnt < V (0 beyond the end)
   const int64_t groups = (a.P + V - 1) / V;
   const int64_t whole = a.P / V;  // groups with V columns
-  const int64_t span = static_cast<int64_t>(gridDim.x) * nt;
-  const int64_t first = static_cast<int64_t>(blockIdx.x) * nt;
-  const int64_t iters = first < groups ? (groups - first + span - 1) / span : 0;
-  const int64_t full_iters =
-      first + nt <= whole ? (iters < (whole - first - nt) / span + 1 ? iters : (whole - first - nt) / span + 1) : 0;
-  auto column = [&](int64_t it) { return (first + it * span + tid) * V; };
+  const int64_t steps_total = (groups + nt - 1) / nt;
+  const int64_t per = a.tile_groups / nt;
+  const int64_t t0 = static_cast<int64_t>(blockIdx.x) * per;
+  const int64_t steps_left = steps_total - t0;
+  const int64_t iters = steps_left <= 0 ? 0 : (steps_left < per ? steps_left : per);
+  const int64_t full_left = whole / nt - t0;  // steps of this workgroup with every thread full
+  const int64_t full_iters = full_left <= 0 ? 0 : (full_left < iters ? full_left : iters);
+  auto column = [&](int64_t it) { return ((t0 + it) * nt + tid) * V; };
 
   Staged<DT, V, R> A, B;
   CeSums<V> cs;

@@ -23,7 +23,8 @@ using gasloc::kMaxReplicas;
 namespace {
 
 constexpr int kStageSlots = 4;      // pinned CSR staging slots, reused round-robin
-constexpr int kMaxGridBlocks = 16384;
+constexpr size_t kPartialWords =
+    2 * static_cast<size_t>(gasloc::kMaxPartials) + 2 * (gasloc::kMaxPartials / gasloc::kFinalizeSegment);
 
 thread_local std::string g_thread_error;
 
@@ -51,6 +52,8 @@ size_t plan_stage_bytes(int n) { return sizeof(int32_t) * gasloc::plan_words_max
 size_t stage_bytes(int n) { return std::max(csr_stage_bytes(n), plan_stage_bytes(n)); }
 
 }  // namespace
+
+void gasloc::set_thread_error(const std::string& msg) { g_thread_error = msg; }
 
 struct gasloc_ctx {
   int n = 0;
@@ -80,12 +83,12 @@ struct gasloc_ctx {
   hipEvent_t stage_done[kStageSlots] = {};
   bool stage_used[kStageSlots] = {};
   int stage_next = 0;
-  double* d_partials = nullptr;  // [2 * partial_cap]: consensus error, then pseudo-gradient partials
-  int partial_cap = 0;
+  // [kPartialWords]: consensus-error partials, pseudo-gradient partials (each
+  // kMaxPartials), then the finalize's segment sums
+  double* d_partials = nullptr;
   double* d_ce = nullptr;  // [2]: consensus error, squared pseudo-gradients of the last round
   double* h_ce = nullptr;  // [2] pinned
 
-  int adam_blocks_total = 0;
   int reduce_blocks = 0;
   size_t lds_per_block_max = 0;
   size_t lds_per_cu = 0;
@@ -187,25 +190,23 @@ gasloc::LaunchShape pick_gossip_shape(const gasloc_ctx& c, int nnz) {
   for (int vec : {4, 2, 1}) {
     if (vec > widest) continue;
     for (int threads : {256, 128, 64}) {
-      gasloc::LaunchShape s{vec, threads, 0, 8};
+      gasloc::LaunchShape s{vec, threads, 0, 8, 0};
       if (gasloc::gossip_lds_bytes(c.n, nnz, s) + gasloc::kStaticLds <= budget) return s;
     }
   }
-  return gasloc::LaunchShape{1, 64, 0, 8};
+  return gasloc::LaunchShape{1, 64, 0, 8, 0};
 }
 
-// Grid of a round kernel: one workgroup per resident slot on every CU (the
-// kernels loop over their columns), no more than the columns need.  The
-// residency comes from the occupancy of the exact kernel that runs, so a
-// kernel limited by registers rather than LDS is not given a second, partial
-// wave of workgroups.
+// Residency of a round kernel, used to pick the planned kernel's workgroup
+// size (the one that keeps the most waves per CU).  It comes from the
+// occupancy of the exact kernel that runs (registers, LDS, waves).
 //
 // LDS is given to a workgroup in granules of 1/128 of the CU's LDS (1280 B
 // on MI355X).  The occupancy query counts LDS more finely and over-counts
 // LDS-bound residency: measured on the n=32 random 3-regular workload, 128-
-// and 64-thread workgroups whose LDS rounds up to one more granule ran a
-// partial second wave (30 ms instead of 20 ms) exactly in the rounds the
-// granule count predicts, so the LDS bound is applied here as well.
+// and 64-thread workgroups whose LDS rounds up to one more granule held one
+// workgroup fewer than the query said, so the LDS bound is applied here as
+// well.
 int lds_blocks_per_cu(const gasloc_ctx& c, size_t dyn_lds) {
   const size_t granule = std::max<size_t>(c.lds_per_cu / 128, 1);
   const size_t held = (dyn_lds + gasloc::kStaticLds + granule - 1) / granule * granule;
@@ -221,27 +222,49 @@ int resident_blocks_per_cu(const gasloc_ctx& c, const gasloc::LaunchShape& s, bo
   return std::max(1, query <= 0 ? by_lds : std::min(query, by_lds));  // a failed query leaves the LDS bound
 }
 
-int round_blocks(const gasloc_ctx& c, const gasloc::LaunchShape& s, bool fused, bool planned, size_t dyn_lds) {
-  const int per_cu = resident_blocks_per_cu(c, s, fused, planned, dyn_lds);
-  const int64_t groups = (c.P + s.vec - 1) / s.vec;
-  const int64_t needed = (groups + s.threads - 1) / s.threads;
-  return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(needed, int64_t(c.cus) * per_cu)));
+// Grid of a round kernel: the columns are cut into steps of threads * vec
+// columns, and workgroup b takes `per` consecutive steps, one after the other,
+// then exits.  The grid is not persistent: workgroups are dispatched in column
+// order, so the columns in flight form one compact window sweeping the rows
+// once (as for the AdamW kernel; a grid-stride loop over a fixed grid spreads
+// them over whole rows as its workgroups drift apart).  A few steps per
+// workgroup amortise its start (CSR staging, barrier) and its reduction:
+// measured on MI355X (gossip round alone), per = 8 against 1 took n=16,
+// P=350M from 26.9 to 25.6 ms and n=64, P=50M from 10.7 to 10.4 ms, while 64
+// was slower again (26.3, 10.8 ms).  So per = 8, less where that would leave
+// fewer than 16 workgroups per CU (n=4, P=1M: 0.031 ms at per = 1, 0.061 at
+// 8), and more only if the partials buffer requires it.
+void tile_grid(const gasloc_ctx& c, gasloc::LaunchShape* s) {
+#ifdef GASLOC_TUNING
+  if (const char* env = std::getenv("GASLOC_GOSSIP_PER")) s->per = std::max(0, std::atoi(env));
+#endif
+  const int64_t groups = (c.P + s->vec - 1) / s->vec;
+  const int64_t steps = (groups + s->threads - 1) / s->threads;
+  int64_t per = s->per > 0 ? s->per : std::min<int64_t>(8, std::max<int64_t>(1, steps / (16 * int64_t(c.cus))));
+  per = std::max<int64_t>(per, (steps + gasloc::kMaxPartials - 1) / gasloc::kMaxPartials);
+  s->per = static_cast<int>(per);
+  s->blocks = static_cast<int>(std::max<int64_t>(1, (steps + per - 1) / per));
 }
 
-// Optional shape override for tuning sweeps:
-// GASLOC_GOSSIP_SHAPE="vec,threads,blocks,batch" (blocks 0 = computed).
+// Shape override for tuning sweeps, compiled only into a library built with
+// -DGASLOC_TUNING: GASLOC_GOSSIP_SHAPE="vec,threads,per,batch" (per 0 =
+// computed).  The default build reads no environment here.
 void apply_shape_override(gasloc::LaunchShape* s) {
+#ifndef GASLOC_TUNING
+  (void)s;
+#else
   const char* env = std::getenv("GASLOC_GOSSIP_SHAPE");
   if (!env) return;
-  int v = 0, t = 0, b = 0, r = 0;
-  if (std::sscanf(env, "%d,%d,%d,%d", &v, &t, &b, &r) == 4 && (v == 1 || v == 2 || v == 4) &&
-      (t == 64 || t == 128 || t == 256) && b >= 0 && b <= kMaxGridBlocks &&
+  int v = 0, t = 0, per = 0, r = 0;
+  if (std::sscanf(env, "%d,%d,%d,%d", &v, &t, &per, &r) == 4 && (v == 1 || v == 2 || v == 4) &&
+      (t == 64 || t == 128 || t == 256) && per >= 0 && per <= (1 << 20) &&
       (r == 1 || r == 2 || r == 4 || r == 8)) {
     s->vec = v;
     s->threads = t;
-    s->blocks = b;
+    s->per = per;
     s->batch = r;
   }
+#endif
 }
 
 void release(gasloc_ctx* c) {
@@ -330,7 +353,8 @@ gasloc_status upload_plan(gasloc_ctx* c, const std::vector<int32_t>& ops) {
 // n <= 16 the phase kernel keeps more loads in flight and the two tie, except
 // the fused round (n=16 one-peer exponential: 44.8 vs 45.4 ms) and the
 // complete graph (n=16: 29.8 vs 26.1 ms).
-// Override for tuning sweeps: GASLOC_GOSSIP_KERNEL=phase|planned.
+// Test hook (documented in gasloc.h): GASLOC_GOSSIP_KERNEL=phase|planned forces
+// one kernel, so that the test suite can run every case through both.
 bool use_planned_kernel(const gasloc_ctx& c) {
   if (const char* env = std::getenv("GASLOC_GOSSIP_KERNEL")) {
     if (std::strcmp(env, "phase") == 0) return false;
@@ -454,13 +478,13 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
     // 256 threads for 14-15 slots (5 workgroups, 20 waves, 19.3-19.5 ms) and
     // 128 threads for 16-19 slots (8-9 workgroups, 16-18 waves, 20.5 ms
     // against 21.5-22.0 ms with 4 workgroups of 256).
-    shape = gasloc::LaunchShape{slots <= 8 ? 4 : 2, 256, 0, gasloc::kPlanBatch};
+    shape = gasloc::LaunchShape{slots <= 8 ? 4 : 2, 256, 0, gasloc::kPlanBatch, 0};
     {
       int best_waves = -1;
       gasloc::LaunchShape best = shape;
       for (int vec = shape.vec; vec >= 1 && best_waves < 0; vec /= 2) {
         for (int threads : {256, 128, 64}) {
-          gasloc::LaunchShape s{vec, threads, 0, gasloc::kPlanBatch};
+          gasloc::LaunchShape s{vec, threads, 0, gasloc::kPlanBatch, 0};
           const size_t dyn = gasloc::planned_lds_bytes(slots, s);
           if (dyn + gasloc::kStaticLds > std::min(c->lds_per_cu / 2, c->lds_per_block_max)) continue;
           const int waves = resident_blocks_per_cu(*c, s, step != nullptr, true, dyn) * (threads / 64);
@@ -474,18 +498,14 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
     }
     apply_shape_override(&shape);
     lds = gasloc::planned_lds_bytes(slots, shape) + gasloc::kStaticLds;
-    if (shape.blocks == 0)
-      shape.blocks = round_blocks(*c, shape, step != nullptr, true, gasloc::planned_lds_bytes(slots, shape));
   } else {
     shape = pick_gossip_shape(*c, nnz);
     if (step) shape.batch = 4;
     apply_shape_override(&shape);
     if (step && shape.batch == 8) shape.batch = 4;  // the fused kernel batches at most 4 workers
     lds = gasloc::gossip_lds_bytes(c->n, nnz, shape) + gasloc::kStaticLds;
-    if (shape.blocks == 0)
-      shape.blocks = round_blocks(*c, shape, step != nullptr, false, gasloc::gossip_lds_bytes(c->n, nnz, shape));
   }
-  shape.blocks = std::min(shape.blocks, c->partial_cap);
+  tile_grid(*c, &shape);
   if (lds > c->lds_per_block_max) return fail(c, GASLOC_EINVAL, "gossip shape exceeds the device's LDS per workgroup");
   gasloc_status st = planned ? upload_plan(c, c->plan_ops) : upload_csr(c, rp, col, val, nnz);
   if (st != GASLOC_OK) return st;
@@ -501,6 +521,7 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
   a.val = reinterpret_cast<const float*>(c->d_csr + rp_bytes + sizeof(int32_t) * c->n * c->n);
   a.ld = c->buf.ld;
   a.P = c->P;
+  a.tile_groups = static_cast<int64_t>(shape.per) * shape.threads;
   a.n = c->n;
   a.nnz = nnz;
   a.mu = c->hp.outer_momentum;
@@ -528,7 +549,7 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
     std::memcpy(a.c2, step->c2, sizeof a.c2);
   }
   a.partials = c->d_partials;
-  a.pg_partials = c->d_partials + c->partial_cap;
+  a.pg_partials = c->d_partials + gasloc::kMaxPartials;
   if (planned) {
     a.ops = reinterpret_cast<const int32_t*>(c->d_csr);
     a.slots = slots;
@@ -538,7 +559,8 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
     HIP_TRY(c, gasloc::launch_gossip_round(a, c->hp.param_dtype, step != nullptr, c->hp.round_form, shape,
                                            c->stream));
   }
-  HIP_TRY(c, gasloc::launch_finalize2(c->d_partials, a.pg_partials, shape.blocks, c->d_ce, c->stream));
+  HIP_TRY(c, gasloc::launch_finalize2_large(c->d_partials, a.pg_partials, shape.blocks,
+                                             c->d_partials + 2 * gasloc::kMaxPartials, c->d_ce, c->stream));
   if (step) {
     for (int i = 0; i < c->n; ++i)
       if ((step->active >> i) & 1ull) c->k[static_cast<size_t>(i)] += 1;
@@ -619,10 +641,11 @@ gasloc_status gasloc_init(int32_t n, int64_t P, const gasloc_topology* topology,
     }
   }
 
+  // an allocation that runs out of memory is ENOMEM, any other HIP failure EDEVICE
   auto init_fail = [&](hipError_t e, const char* what) {
     g_thread_error = format("%s: %s", what, hipGetErrorString(e));
     release(c);
-    return GASLOC_EDEVICE;
+    return e == hipErrorOutOfMemory ? GASLOC_ENOMEM : GASLOC_EDEVICE;
   };
   hipError_t e = hipGetDevice(&c->device);
   if (e != hipSuccess) return init_fail(e, "hipGetDevice");
@@ -640,14 +663,10 @@ gasloc_status gasloc_init(int32_t n, int64_t P, const gasloc_topology* topology,
     release(c);
     return fail(nullptr, GASLOC_EINVAL, "gossip workgroup does not fit the device's LDS");
   }
-  // at least two 256-thread workgroups per CU and 32 per active worker:
-  // measured best for the AdamW stream on the n = 8..64 workloads
-  c->adam_blocks_total = c->cus * 2;
-  c->reduce_blocks = std::min(kMaxGridBlocks, c->cus * 4);
-  c->partial_cap = kMaxGridBlocks;
+  c->reduce_blocks = c->cus * 4;
 
   if ((e = hipMalloc(&c->d_csr, stage_bytes(n))) != hipSuccess) return init_fail(e, "hipMalloc csr");
-  if ((e = hipMalloc(&c->d_partials, 2 * sizeof(double) * c->partial_cap)) != hipSuccess)
+  if ((e = hipMalloc(&c->d_partials, sizeof(double) * kPartialWords)) != hipSuccess)
     return init_fail(e, "hipMalloc partials");
   if ((e = hipMalloc(&c->d_ce, 2 * sizeof(double))) != hipSuccess) return init_fail(e, "hipMalloc ce");
   if ((e = hipHostMalloc(&c->h_ce, 2 * sizeof(double), hipHostMallocDefault)) != hipSuccess)
@@ -708,19 +727,7 @@ gasloc_status gasloc_local_step(gasloc_ctx* c, const float* grads, int64_t grad_
     ++slots;
   }
   a.n_active = slots;
-  const int64_t groups = (c->P + 3) / 4;
-  int total_blocks = c->adam_blocks_total;
-  int64_t floor_per_worker = 32;
-  if (const char* env = std::getenv("GASLOC_ADAM_BLOCKS")) {  // tuning sweeps
-    const int b = std::atoi(env);
-    if (b > 0 && b <= 1 << 20) {
-      total_blocks = b;
-      floor_per_worker = 1;
-    }
-  }
-  const int64_t want = std::max<int64_t>(floor_per_worker, total_blocks / slots);
-  const int per_worker = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(want, (groups + 255) / 256)));
-  HIP_TRY(c, gasloc::launch_local_adamw(a, c->hp.param_dtype, per_worker, c->stream));
+  HIP_TRY(c, gasloc::launch_local_adamw(a, c->hp.param_dtype, c->stream));
   commit_step(c, plan);
   return GASLOC_OK;
 }

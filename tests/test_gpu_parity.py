@@ -76,6 +76,9 @@ SMALL = [
     (8, 10007, "exponential", "f32", 1, 0.1, 0.9, False),
     (16, 8191, "one_peer_exp", "f32", 2, 0.1, 0.0, False),
     (32, 3001, "random_regular", "bf16", 2, 0.1, 0.9, True),
+    # fp32 rows of four entries (3-regular graph with its self-loop) take the
+    # planned kernel's branch-free sum at 2 columns per thread; ragged P
+    (32, 4097, "random_regular", "f32", 2, 0.1, 0.9, True),
     (33, 515, "two_peer", "f32", 1, 0.3, 0.5, True),
     (64, 2053, "complete", "f32", 1, 0.0, 0.9, True),
     (64, 4099, "one_peer", "bf16", 2, 0.0, 0.9, True),
@@ -604,6 +607,12 @@ def test_maximum_row_length_64bit_offsets():
         pair.local_step()
         pair.local_step()
         pair.gossip_round(t)
+        # the round's own consensus error: 2^21 steps of 1024 columns, two per
+        # workgroup, 2^20 partials summed in segments; the standalone reduction
+        # of the same x groups the fp64 sums differently
+        fused = pair.gpu.consensus_error()
+        whole = pair.gpu.consensus_error_cols(0, P)
+        assert abs(fused - whole) <= 1e-12 * abs(whole), (fused, whole)
         tail = pair.gpu.consensus_error_cols(P - 64, P)
         reduction_close(tail, pair.oracles["f32"].consensus_error(slice(len(cols) - 64, len(cols))), "tail CE")
     pair.check_state(tag="max row length")
