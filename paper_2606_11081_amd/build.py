@@ -1,8 +1,11 @@
 """Compile libgasloc.so (HIP kernels for gfx950 + host runtime) in-tree.
 
 Every HIP translation unit is built with -ffp-contract=off (no fused
-multiply-add: the op order of the round is part of its definition) and with
-packed-fp32 instructions disabled.
+multiply-add: the op order of the round is part of its definition).  A .hip
+file is compiled in two passes: the device pass for gfx950 with packed-fp32
+instructions disabled (a gfx950 target feature), then the host pass, which
+embeds the device binary and is not given that feature (the host target does
+not know it).
 """
 import os
 import subprocess
@@ -14,14 +17,14 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libgasloc.so")
-SOURCES = ["adamw.hip", "round_phase.hip", "round_planned.hip", "reductions.hip", "runtime.cpp", "topology.cpp",
-           "schedule.cpp", "plan.cpp"]
+SOURCES = ["adamw.hip", "round_phase.hip", "round_planned.hip", "reductions.hip", "stream_probe.hip", "runtime.cpp",
+           "topology.cpp", "schedule.cpp", "plan.cpp"]
 ARCH = "gfx950"
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-ffp-contract=off",
           "-I", os.path.join(ROOT, "include"), "-I", CSRC]
-DEVICE = ["-x", "hip", "--offload-arch=" + ARCH, "-Xclang", "-target-feature", "-Xclang",
-          "-packed-fp32-ops", "-fno-gpu-rdc"]
+HIP = ["-x", "hip", "--offload-arch=" + ARCH, "-fno-gpu-rdc"]
+DEVICE_ONLY = ["--cuda-device-only", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
@@ -29,16 +32,27 @@ HOST_CXX = [os.path.join(ROCM, "llvm", "bin", "clang++"), "-D__HIP_PLATFORM_AMD_
             "-I", os.path.join(ROCM, "include")]
 
 
-def _compile(src, verbose):
-    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    if src.endswith(".hip"):
-        cmd = ["hipcc"] + COMMON + DEVICE
-    else:  # host-only C++ against the HIP runtime API
-        cmd = HOST_CXX + COMMON
-    cmd += ["-c", os.path.join(CSRC, src), "-o", obj]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
+
+
+def device_binary(src):
+    """The bundled gfx950 code object of a .hip source (written by build())."""
+    return os.path.join(BUILD, os.path.splitext(src)[0] + ".hipfb")
+
+
+def _compile(src, verbose):
+    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+    path = os.path.join(CSRC, src)
+    if src.endswith(".hip"):
+        fatbin = device_binary(src)
+        _run(["hipcc"] + COMMON + HIP + DEVICE_ONLY + ["-c", path, "-o", fatbin], verbose)
+        _run(["hipcc"] + COMMON + HIP + ["--cuda-host-only", "-Xclang", "-fcuda-include-gpubinary", "-Xclang",
+                                         fatbin, "-c", path, "-o", obj], verbose)
+    else:  # host-only C++ against the HIP runtime API
+        _run(HOST_CXX + COMMON + ["-c", path, "-o", obj], verbose)
     return obj
 
 
@@ -47,10 +61,7 @@ def build(verbose=False):
     with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
         objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
     tmp = LIB + ".tmp"
-    cmd = ["hipcc", "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
+    _run(["hipcc", "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs, verbose)
     os.replace(tmp, LIB)
     return LIB
 
