@@ -4,7 +4,18 @@ One step = one whole round of the hot path on resident synthetic replicas:
 H_i masked local AdamW steps, the fused gossip round (pseudo-gradient, outer
 Nesterov step, neighbour mix, consensus momentum, consensus-error partials),
 its fp64 finalize and the consensus-error readback.  `value` is
-replica-param updates per second, n * P / (seconds per round).
+replica-param updates per second, n * P / (seconds per round), on the
+headline workload (n=16, P=350M by default).
+
+After the headline workload, the other workloads of the benchmark run one
+after another in the same process (each one's buffers freed before the
+next), each with its own rounds, standalone gossip round, streaming-probe
+mixes and oracle baselines, reported under "workloads".
+
+Gradients: one resident [n, ld] fp32 batch per workload, drawn once before
+timing (seed 2); every local step reads it from HBM, so each step moves the
+bytes of a fresh gradient batch (the stand-in for backpropagation, which is
+not part of the round).
 
 Prints ONE JSON line.  Per-kernel durations come from HIP events recorded on
 the library's stream around every call inside the timed region.
@@ -21,6 +32,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, AMD specification
+INFINITY_CACHE_BYTES = 256e6  # MI355X last-level cache
 METRIC = "replica-param updates/s per gossip round; achieved HBM GB/s vs peak"
 DEFAULT_WORKLOAD = "onepeer-exp-n16-p350m"
 
@@ -97,10 +109,14 @@ def fused_bytes_per_rp(sp, gamma, active, stepped, with_u=True, form="eq"):
     return b
 
 
+def pmc_profile(kernel, workload):
+    return os.path.join("profiles", "%s_%s_pmc.md" % (kernel, workload))  # kernel: a kernel or role name
+
+
 def read_traffic(kernel, workload, n):
     """HBM bytes per dispatch from a committed rocprofv3 --pmc summary, or None
     if absent or taken on other sources of the kernel's family."""
-    path = os.path.join(ROOT, "profiles", "%s_%s_pmc.md" % (kernel, workload))  # kernel: a kernel or role name
+    path = os.path.join(ROOT, pmc_profile(kernel, workload))
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -108,6 +124,17 @@ def read_traffic(kernel, workload, n):
     if not m or m.group(2) != kernels_sha(kernel_family(kernel, n)):
         return None
     return float(m.group(1))
+
+
+def traffic_source(kernel, workload, n):
+    """Where a reported traffic figure comes from (None when there is none):
+    not measured in this run, but read from a committed counter summary whose
+    kernel sources are the ones built now."""
+    if read_traffic(kernel, workload, n) is None:
+        return None
+    return {"profile": pmc_profile(kernel, workload), "kernels_sha": kernels_sha(kernel_family(kernel, n)),
+            "method": "rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE, per dispatch, each scaled by the same "
+                      "counter of the streaming probe's copy of known size (in that profile's process)"}
 
 
 def _oracle_sample(w, columns, form, seed):
@@ -233,16 +260,217 @@ def host_cpu():
     return "unknown CPU"
 
 
+# Streaming-probe mixes (include/gasloc_probe.h): (fp32 reads, bf16 reads,
+# fp32 writes, bf16 writes), destinations in place of the first sources.
+PROBE_MIXES = {
+    "read": (4, 0, 0, 0), "write": (0, 0, 3, 0), "copy": (1, 0, 1, 0),
+    "r16w12_f32": (4, 0, 3, 0),          # AdamW fp32; EQ round fp32, gamma != 0
+    "r12w8_f32": (3, 0, 2, 0),           # EQ round fp32, gamma = 0
+    "adamw_bf16": (3, 1, 2, 1), "round_bf16": (2, 2, 2, 1),
+    "fused_f32": (7, 0, 5, 0), "fused_f32_g0": (6, 0, 4, 0), "fused_bf16": (5, 2, 4, 1),
+}
+PROBE_COUNT = 1 << 28  # elements per stream: 1 GiB per fp32 stream
+
+
+def probe_mix_bytes(mix, count=PROBE_COUNT):
+    r32, r16, w32, w16 = mix
+    return count * (4 * (r32 + w32) + 2 * (r16 + w16))
+
+
+def kernel_mixes(param_dtype, gamma):
+    """The probe mix whose bytes per element match each kernel (EQ form)."""
+    if param_dtype == "bf16":
+        return {"adamw": "adamw_bf16", "round": "round_bf16", "fused": "fused_bf16"}
+    if gamma != 0.0:
+        return {"adamw": "r16w12_f32", "round": "r16w12_f32", "fused": "fused_f32"}
+    return {"adamw": "r16w12_f32", "round": "r12w8_f32", "fused": "fused_f32_g0"}
+
+
+def stream_probe(names, dev, reps=5):
+    """GB/s of the hand-written streaming kernel on each named mix, in this
+    process: one warm-up and `reps` timed launches (median)."""
+    import numpy as np
+    import torch
+
+    import paper_2606_11081_amd as g
+
+    need32 = max(max(PROBE_MIXES[k][0], PROBE_MIXES[k][2]) for k in names)
+    need16 = max(max(PROBE_MIXES[k][1], PROBE_MIXES[k][3]) for k in names)
+    f32 = [torch.ones(PROBE_COUNT, dtype=torch.float32, device=dev) for _ in range(need32)]
+    b16 = [torch.ones(PROBE_COUNT, dtype=torch.bfloat16, device=dev) for _ in range(need16)]
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    out = {}
+    for name in names:
+        r32, r16, w32, w16 = mix = PROBE_MIXES[name]
+        src, dst = f32[:r32] + b16[:r16], f32[:w32] + b16[:w16]
+        ms = []
+        for k in range(reps + 1):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            g.gasloc.gasloc_stream_probe(r32, r16, w32, w16, src, dst, PROBE_COUNT, sink, stream)
+            b.record(stream)
+            torch.cuda.synchronize()
+            if k:
+                ms.append(a.elapsed_time(b))
+        t = float(np.median(ms))
+        out[name] = {"mix": list(mix), "bytes": probe_mix_bytes(mix), "ms": round(t, 4),
+                     "GBps": round(probe_mix_bytes(mix) / (t * 1e-3) / 1e9, 1)}
+    del f32, b16, sink
+    torch.cuda.empty_cache()
+    return out
+
+
+def run_workload(w, form, steps, warmup, fuse, dev, log_prefix="bench"):
+    """Whole rounds of one workload on the GPU: `warmup` untimed rounds, then
+    `steps` timed rounds, then 5 standalone gossip rounds.  Returns the
+    measurements; frees the workload's buffers before returning."""
+    import numpy as np
+    import torch
+
+    import gasloc_inputs as gi
+    import paper_2606_11081_amd as g
+
+    gamma = w.gamma if form == "eq" else 0.0  # the consensus momentum exists in EQ only
+    H_i = gi.local_steps(w)
+    masks = gi.active_masks(H_i)
+    sp = param_bytes(w.param_dtype)
+    log("%s: %s%s  (n=%d P=%d %s H=%s gamma=%g)" % (log_prefix, w.name, "" if form == "eq" else " " + form, w.n,
+                                                   w.P, w.param_dtype,
+                                                   "U{%d..%d}" % w.hetero_H if w.hetero_H else w.H, gamma))
+    lib = g.GASLoC(w.n, w.P, topology=w.topology, seed=gi.SEED_TOPOLOGY, degree=w.degree,
+                   param_dtype=w.param_dtype, beta1=gi.BETA1, beta2=gi.BETA2, eps=gi.EPS,
+                   weight_decay=gi.WEIGHT_DECAY, outer_lr=gi.OUTER_LR, outer_momentum=gi.OUTER_MOMENTUM,
+                   outer_nesterov=True, consensus_momentum=gamma, round_form=form)
+    lib.set_params(gi.make_x0(w.P, device=dev))
+    grads = torch.empty((w.n, lib.ld), dtype=torch.float32, device=dev)
+    gi.fill_grads(grads, gi.worker_means(w.n), 0)
+    stream = lib.stream
+    torch.cuda.synchronize()
+
+    def rec(ev, key, extra=None):
+        pair = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True), extra)
+        ev[key].append(pair)
+        pair[0].record(stream)
+        return pair
+
+    def one_round(t, ev=None):
+        """H_i local steps and the round; the last step is fused into the round."""
+        last = len(masks) - 1 if fuse else len(masks)
+        for h in range(last):
+            e = rec(ev, "adam", int(masks[h].sum())) if ev is not None else None
+            lib.local_step(grads, gi.LOCAL_LR, masks[h])
+            if e:
+                e[1].record(stream)
+        if fuse:
+            e = rec(ev, "round", masks[-1]) if ev is not None else None
+            lib.local_step_gossip_round(grads, gi.LOCAL_LR, t, masks[-1])
+        else:
+            e = rec(ev, "round", None) if ev is not None else None
+            lib.gossip_round(t)
+        if e:
+            e[1].record(stream)
+        return lib.consensus_error()
+
+    for t in range(warmup):
+        one_round(t)
+    torch.cuda.synchronize()
+
+    ev = {"adam": [], "round": []}
+    ces = []
+    wall = []  # per round: each round ends with the blocking consensus-error readback
+    t0 = time.perf_counter()
+    for s in range(steps):
+        r0 = time.perf_counter()
+        ces.append(one_round(warmup + s, ev))
+        wall.append((time.perf_counter() - r0) * 1e3)
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) / steps * 1e3
+
+    adam_ms = [a.elapsed_time(b) for a, b, _ in ev["adam"]]
+    adam_rp = [k * w.P for _, _, k in ev["adam"]]
+    round_ms = [a.elapsed_time(b) for a, b, _ in ev["round"]]
+    adam_bytes = adamw_bytes_per_rp(sp)
+    if fuse:
+        act_last = masks[-1]
+        # a worker read y in the fused call if it took a local step earlier this round
+        stepped_before = np.minimum(H_i, len(masks) - 1) > 0
+        round_bytes = sum(fused_bytes_per_rp(sp, gamma, bool(act_last[i]), bool(stepped_before[i]), form=form)
+                          for i in range(w.n)) * w.P
+    else:
+        round_bytes = w.n * w.P * gossip_bytes_per_rp(sp, gamma, form=form)
+    adam_gbps = sum(r * adam_bytes for r in adam_rp) / (sum(adam_ms) * 1e-3) / 1e9 if adam_ms else 0.0
+    round_gbps = round_bytes / (np.mean(round_ms) * 1e-3) / 1e9
+
+    # the standalone gossip kernel (no fused step), timed after the rounds
+    g_ms = []
+    for s in range(5):
+        lib.local_step(grads, gi.LOCAL_LR)
+        e = rec({"g": []}, "g")
+        lib.gossip_round(warmup + steps + s)
+        e[1].record(stream)
+        torch.cuda.synchronize()
+        g_ms.append(e[0].elapsed_time(e[1]))
+    gossip_bytes = gossip_bytes_per_rp(sp, gamma, form=form)
+    gossip_ms = float(np.median(g_ms))
+    gossip_gbps = w.n * w.P * gossip_bytes / (gossip_ms * 1e-3) / 1e9
+    lib.close()
+    del lib, grads
+    torch.cuda.empty_cache()
+    return {
+        "H_i": H_i, "gamma": gamma, "ms_per_step": ms_step, "wall": wall, "ces": ces,
+        "adam_ms": adam_ms, "adam_rp": adam_rp, "adam_bytes": adam_bytes, "adam_gbps": adam_gbps,
+        "round_ms": round_ms, "round_bytes": round_bytes, "round_gbps": round_gbps,
+        "gossip_ms": gossip_ms, "gossip_bytes": gossip_bytes, "gossip_gbps": gossip_gbps,
+    }
+
+
+def frac(x, ref):
+    return round(x / ref, 4) if ref else None
+
+
+def kernel_records(w, form, fuse, r, probe):
+    """The per-kernel records of one workload: time, GB/s, fraction of peak and
+    of the matching streaming-probe mix."""
+    import numpy as np
+
+    mixes = kernel_mixes(w.param_dtype, r["gamma"]) if form == "eq" else {}
+    pg = lambda role: probe.get(mixes.get(role), {}).get("GBps")  # noqa: E731
+    round_role = "fused" if fuse else "round"
+    return {
+        "gossip_round": {"role": "gossip round alone (library-chosen gossip kernel + CSR/plan upload + finalize)",
+                         "rp_updates_per_s": w.n * w.P / (r["gossip_ms"] * 1e-3),
+                         "ms": round(r["gossip_ms"], 4), "GBps": round(r["gossip_gbps"], 1),
+                         "frac_of_peak": frac(r["gossip_gbps"], PEAK_HBM_GBPS), "bytes_per_rp": r["gossip_bytes"],
+                         "probe_mix": mixes.get("round"), "frac_of_probe": frac(r["gossip_gbps"], pg("round"))},
+        "round_kernel": {"role": "fused_round" if fuse else "gossip_round",
+                         "ms": round(float(np.mean(r["round_ms"])), 4), "GBps": round(r["round_gbps"], 1),
+                         "frac_of_peak": frac(r["round_gbps"], PEAK_HBM_GBPS),
+                         "bytes_per_launch": int(r["round_bytes"]), "probe_mix": mixes.get(round_role),
+                         "frac_of_probe": frac(r["round_gbps"], pg(round_role))},
+        "local_adamw": {"ms_per_launch": round(float(np.mean(r["adam_ms"])), 4) if r["adam_ms"] else None,
+                        "GBps": round(r["adam_gbps"], 1), "frac_of_peak": frac(r["adam_gbps"], PEAK_HBM_GBPS),
+                        "bytes_per_rp": r["adam_bytes"],
+                        "launches_per_round": len(r["adam_ms"]) // max(len(r["wall"]), 1),
+                        "probe_mix": mixes.get("adamw") if r["adam_ms"] else None,
+                        "frac_of_probe": frac(r["adam_gbps"], pg("adamw")) if r["adam_ms"] else None},
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--workloads", default="auto",
+                    help="other workloads timed after the headline one: 'auto' (all the others when the headline is "
+                         "the default workload in the EQ form, else none), 'none', or a comma-separated list")
+    ap.add_argument("--workload-steps", type=int, default=5, help="timed rounds of each other workload")
     ap.add_argument("--cpu-columns", type=int, default=0,
                     help="columns of the oracle's sample (0: sized to about 12 s of single-core work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--copy-gb", type=float, default=8.0, help="size of the copy probe (GB read)")
+    ap.add_argument("--no-probe", dest="probe", action="store_false", help="skip the streaming-probe mixes")
     ap.add_argument("--no-fuse", dest="fuse", action="store_false",
                     help="run the last local step and the round as two calls")
     ap.add_argument("--form", choices=FORMS, default="eq",
@@ -260,133 +488,43 @@ def main():
     import torch
 
     import gasloc_inputs as gi
-    import paper_2606_11081_amd as g
 
     w = gi.WORKLOADS[args.workload]
-    gamma = w.gamma if args.form == "eq" else 0.0  # the consensus momentum exists in EQ only
     # profiles and the JSON name the workload with its round form when not EQ
     wname = w.name if args.form == "eq" else "%s-%s" % (w.name, args.form)
-    H_i = gi.local_steps(w)
-    masks = gi.active_masks(H_i)
-    sp = param_bytes(w.param_dtype)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    log("bench: %s  (n=%d P=%d %s H=%s gamma=%g)" % (wname, w.n, w.P, w.param_dtype,
-                                                    "U{%d..%d}" % w.hetero_H if w.hetero_H else w.H, gamma))
+    r = run_workload(w, args.form, args.steps, args.warmup, args.fuse, dev)
+    gamma, H_i = r["gamma"], r["H_i"]
+    probe = {}
+    if args.probe:
+        names = ["read", "write", "copy"] + sorted(set(kernel_mixes(w.param_dtype, gamma).values()))
+        log("bench: streaming probe, mixes %s" % ", ".join(names))
+        probe = stream_probe(names, dev)
+    recs = kernel_records(w, args.form, args.fuse, r, probe)
 
-    lib = g.GASLoC(w.n, w.P, topology=w.topology, seed=gi.SEED_TOPOLOGY, degree=w.degree,
-                   param_dtype=w.param_dtype, beta1=gi.BETA1, beta2=gi.BETA2, eps=gi.EPS,
-                   weight_decay=gi.WEIGHT_DECAY, outer_lr=gi.OUTER_LR, outer_momentum=gi.OUTER_MOMENTUM,
-                   outer_nesterov=True, consensus_momentum=gamma, round_form=args.form)
-    lib.set_params(gi.make_x0(w.P, device=dev))
-    # one resident gradient batch (stand-in for backpropagated gradients)
-    grads = torch.empty((w.n, lib.ld), dtype=torch.float32, device=dev)
-    gi.fill_grads(grads, gi.worker_means(w.n), 0)
-    stream = lib.stream
-    torch.cuda.synchronize()
-
-    def rec(ev, key, extra=None):
-        pair = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True), extra)
-        ev[key].append(pair)
-        pair[0].record(stream)
-        return pair
-
-    def one_round(t, ev=None):
-        """H_i local steps and the round; the last step is fused into the round."""
-        last = len(masks) - 1 if args.fuse else len(masks)
-        for h in range(last):
-            e = rec(ev, "adam", int(masks[h].sum())) if ev is not None else None
-            lib.local_step(grads, gi.LOCAL_LR, masks[h])
-            if e:
-                e[1].record(stream)
-        if args.fuse:
-            e = rec(ev, "round", masks[-1]) if ev is not None else None
-            lib.local_step_gossip_round(grads, gi.LOCAL_LR, t, masks[-1])
-        else:
-            e = rec(ev, "round", None) if ev is not None else None
-            lib.gossip_round(t)
-        if e:
-            e[1].record(stream)
-        return lib.consensus_error()
-
-    for t in range(args.warmup):
-        one_round(t)
-    torch.cuda.synchronize()
-
-    ev = {"adam": [], "round": []}
-    ces = []
-    torch.cuda.synchronize()
-    wall = []  # per round: each round ends with the blocking consensus-error readback
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        r0 = time.perf_counter()
-        ces.append(one_round(args.warmup + s, ev))
-        wall.append((time.perf_counter() - r0) * 1e3)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    ms_step = elapsed / args.steps * 1e3
-
-    adam_ms = [a.elapsed_time(b) for a, b, _ in ev["adam"]]
-    adam_rp = [k * w.P for _, _, k in ev["adam"]]
-    round_ms = [a.elapsed_time(b) for a, b, _ in ev["round"]]
-    adam_bytes = adamw_bytes_per_rp(sp)
-    if args.fuse:
-        act_last = masks[-1]
-        # a worker read y in the fused call if it took a local step earlier this round
-        stepped_before = np.minimum(H_i, len(masks) - 1) > 0
-        round_bytes = sum(fused_bytes_per_rp(sp, gamma, bool(act_last[i]), bool(stepped_before[i]), form=args.form)
-                          for i in range(w.n)) * w.P
-    else:
-        round_bytes = w.n * w.P * gossip_bytes_per_rp(sp, gamma, form=args.form)
-    adam_gbps = sum(r * adam_bytes for r in adam_rp) / (sum(adam_ms) * 1e-3) / 1e9 if adam_ms else 0.0
-    round_gbps = round_bytes / (np.mean(round_ms) * 1e-3) / 1e9
-    adam_total, round_total = sum(adam_ms), sum(round_ms)
-
-    # the standalone gossip kernel (no fused step), timed after the rounds
-    g_ms = []
-    for s in range(5):
-        lib.local_step(grads, gi.LOCAL_LR)
-        e = rec({"g": []}, "g")
-        lib.gossip_round(args.warmup + args.steps + s)
-        e[1].record(stream)
-        torch.cuda.synchronize()
-        g_ms.append(e[0].elapsed_time(e[1]))
-    gossip_bytes = gossip_bytes_per_rp(sp, gamma, form=args.form)
-    gossip_ms = float(np.median(g_ms))
-    gossip_gbps = w.n * w.P * gossip_bytes / (gossip_ms * 1e-3) / 1e9
-
-    # copy probe: a plain device copy of known size, same run
-    copy_elems = int(args.copy_gb * 1e9 / 4)
-    src = torch.empty(copy_elems, dtype=torch.float32, device=dev).fill_(1.0)
-    dst = torch.empty_like(src)
-    dst.copy_(src)
-    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    c0.record(stream)
-    for _ in range(5):
-        dst.copy_(src)
-    c1.record(stream)
-    torch.cuda.synchronize()
-    copy_gbps = 2 * copy_elems * 4 * 5 / (c0.elapsed_time(c1) * 1e-3) / 1e9
-    del src, dst
-
-    if adam_total >= round_total and adam_ms:
-        dom, dom_bytes = "k_local_adamw", float(np.mean([r * adam_bytes for r in adam_rp]))
-        dom_ms = float(np.mean(adam_ms))
+    adam_total, round_total = sum(r["adam_ms"]), sum(r["round_ms"])
+    if adam_total >= round_total and r["adam_ms"]:
+        dom = "k_local_adamw"
+        dom_bytes = float(np.mean([k * r["adam_bytes"] for k in r["adam_rp"]]))
+        dom_ms = float(np.mean(r["adam_ms"]))
     else:
         dom = "fused_round" if args.fuse else "gossip_round"
-        dom_bytes, dom_ms = round_bytes, float(np.mean(round_ms))
+        dom_bytes, dom_ms = r["round_bytes"], float(np.mean(r["round_ms"]))
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
-                "traffic": read_traffic(dom, wname, w.n),
+                "traffic": read_traffic(dom, wname, w.n), "traffic_source": traffic_source(dom, wname, w.n),
                 "algorithmic_bytes_per_launch": int(dom_bytes), "avg_launch_ms": round(dom_ms, 4)}
+    recs["gossip_round"]["traffic"] = read_traffic("gossip_round", wname, w.n)
+    recs["gossip_round"]["traffic_source"] = traffic_source("gossip_round", wname, w.n)
     out = {
         "metric": METRIC,
-        "value": w.n * w.P / (ms_step * 1e-3),
+        "value": w.n * w.P / (r["ms_per_step"] * 1e-3),
         "unit": "replica-param updates/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 3),
-        "round_ms_p10_p50_p90": [round(float(np.percentile(wall, q)), 3) for q in (10, 50, 90)],
+        "ms_per_step": round(r["ms_per_step"], 3),
+        "round_ms_p10_p50_p90": [round(float(np.percentile(r["wall"], q)), 3) for q in (10, 50, 90)],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         # the arithmetic of every kernel is fp32 (reductions fp64), whatever the
         # parameters are stored in; the storage type is config.param_dtype
@@ -394,32 +532,49 @@ def main():
         "config": {"workload": wname, "n": w.n, "P": w.P, "topology": w.topology, "round_form": args.form,
                    "local_steps": "U{%d..%d}" % w.hetero_H if w.hetero_H else w.H,
                    "gamma": gamma, "param_dtype": w.param_dtype, "state_dtype": "f32",
-                   "last_local_step_fused": bool(args.fuse)},
+                   "last_local_step_fused": bool(args.fuse),
+                   "gradients": "one resident [n, ld] fp32 batch, drawn once (seed 2), read by every local step"},
         "roofline": roofline,
-        "gossip_round": {"role": "gossip round alone (library-chosen gossip kernel + CSR/plan upload + finalize)",
-                         "rp_updates_per_s": w.n * w.P / (gossip_ms * 1e-3),
-                         "ms": round(gossip_ms, 4), "GBps": round(gossip_gbps, 1),
-                         "frac_of_peak": round(gossip_gbps / PEAK_HBM_GBPS, 4), "bytes_per_rp": gossip_bytes,
-                         "traffic": read_traffic("gossip_round", wname, w.n)},
-        "round_kernel": {"role": "fused_round" if args.fuse else "gossip_round",
-                         "ms": round(float(np.mean(round_ms)), 4), "GBps": round(round_gbps, 1),
-                         "frac_of_peak": round(round_gbps / PEAK_HBM_GBPS, 4),
-                         "bytes_per_launch": int(round_bytes)},
-        "local_adamw": {"ms_per_launch": round(float(np.mean(adam_ms)), 4) if adam_ms else None,
-                        "GBps": round(adam_gbps, 1), "frac_of_peak": round(adam_gbps / PEAK_HBM_GBPS, 4),
-                        "bytes_per_rp": adam_bytes, "launches_per_round": len(adam_ms) // max(args.steps, 1)},
-        "copy_probe_GBps": round(copy_gbps, 1),
-        "consensus_error_last": ces[-1],
     }
-    lib.close()
-    del grads
-    torch.cuda.empty_cache()
+    out.update(recs)
+    out["stream_probe"] = probe
+    out["consensus_error_last"] = r["ces"][-1]
     if not args.no_cpu_baseline:
         columns = min(args.cpu_columns, w.P) if args.cpu_columns > 0 else cpu_sample_columns(w, H_i)
         log("bench: timing the oracle on %d columns" % columns)
         out["cpu_baseline"] = cpu_baseline(w, H_i, columns, args.form)
         log("bench: timing the oracle on %d host threads" % host_threads())
         out["cpu_baseline_all_threads"] = cpu_baseline_parallel(w, H_i, columns, args.form)
+
+    if args.workloads == "auto":
+        others = [k for k in gi.WORKLOADS if k != w.name] if (w.name == DEFAULT_WORKLOAD and args.form == "eq") else []
+    elif args.workloads == "none":
+        others = []
+    else:
+        others = [k for k in args.workloads.split(",") if k]
+    if others:
+        out["workloads"] = {}
+    for name in others:
+        wo = gi.WORKLOADS[name]
+        ro = run_workload(wo, "eq", args.workload_steps, 2, True, dev, log_prefix="bench (workloads)")
+        po = {}
+        # a workload whose round fits the 256 MB Infinity Cache is not an HBM
+        # stream: no probe fraction for it
+        if args.probe and wo.n * wo.P * ro["gossip_bytes"] > INFINITY_CACHE_BYTES:
+            po = stream_probe(sorted(set(kernel_mixes(wo.param_dtype, ro["gamma"]).values())), dev)
+        rec = {"n": wo.n, "P": wo.P, "topology": wo.topology, "param_dtype": wo.param_dtype, "gamma": ro["gamma"],
+               "local_steps": "U{%d..%d}" % wo.hetero_H if wo.hetero_H else wo.H,
+               "steps": args.workload_steps, "warmup": 2, "ms_per_step": round(ro["ms_per_step"], 3),
+               "value": wo.n * wo.P / (ro["ms_per_step"] * 1e-3)}
+        rec.update(kernel_records(wo, "eq", True, ro, po))
+        rec["stream_probe"] = po
+        if not args.no_cpu_baseline:
+            Hw = ro["H_i"]
+            columns = max(1, cpu_sample_columns(wo, Hw) // 3)  # about 4 s of single-core work
+            log("bench (workloads): timing the oracle on %d columns of %s" % (columns, name))
+            rec["cpu_baseline"] = cpu_baseline(wo, Hw, columns)
+            rec["cpu_baseline_all_threads"] = cpu_baseline_parallel(wo, Hw, columns)
+        out["workloads"][name] = rec
     print(json.dumps(out), flush=True)
 
 

@@ -1,12 +1,14 @@
 /* A plain C99 consumer of include/gasloc.h, built and run by
  * tests/test_c_header.py against libgasloc.so with no GPU: it uses only the
  * host-side calls (schedules, CSR validation, skipped exchanges, LR
- * schedule) and prints one line per check. */
+ * schedule, the streaming probe's argument checks) and prints one line per
+ * check. */
 #include <math.h>
 #include <stdio.h>
 #include <string.h>
 
 #include "gasloc.h"
+#include "gasloc_probe.h"
 
 int main(void) {
   enum { N = 8, CAP = N * N };
@@ -46,5 +48,9 @@ int main(void) {
 
   printf("lr=%.9g %.9g %.9g\n", gasloc_lr_schedule(1e-3f, 0, 100, 0.1f, 0.01f, 0.0f),
          gasloc_lr_schedule(1e-3f, 10, 100, 0.1f, 0.01f, 0.0f), gasloc_lr_schedule(1e-3f, 99, 100, 0.1f, 0.01f, 0.0f));
+
+  /* rejected before any device work: a mix no kernel has, and a zero count */
+  printf("probe_mix=%d\n", (int)gasloc_stream_probe(1, 1, 1, 1, NULL, NULL, 1024, NULL, NULL));
+  printf("probe_count=%d\n", (int)gasloc_stream_probe(1, 0, 1, 0, NULL, NULL, 0, NULL, NULL));
   return 0;
 }

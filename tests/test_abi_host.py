@@ -16,9 +16,14 @@ KINDS = ["ring", "complete", "exponential", "one_peer_exp", "one_peer", "two_pee
 
 
 def header_functions():
-    text = open(os.path.join(ROOT, "include", "gasloc.h")).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(gasloc_[a-z_]+)\s*\(", text)))
+    """Every function declared by a header under include/."""
+    names = set()
+    inc = os.path.join(ROOT, "include")
+    for h in sorted(os.listdir(inc)):
+        if h.endswith(".h"):
+            text = re.sub(r"/\*.*?\*/", "", open(os.path.join(inc, h)).read(), flags=re.S)
+            names.update(re.findall(r"\b(gasloc_[a-z_]+)\s*\(", text))
+    return sorted(names)
 
 
 def test_library_exports_every_declared_function():
@@ -253,3 +258,32 @@ def test_skip_exchanges_on_a_csr_without_diagonal():
     for a, b in zip(got, exp):
         assert np.array_equal(a, b)
     assert list(got[0]) == [0, 2, 4, 5]
+
+
+@pytest.mark.parametrize("mix,count,msg", [
+    ((1, 1, 1, 1), 1024, "unsupported mix"),
+    ((4, 0, 3, 1), 1024, "unsupported mix"),
+    ((-1, 0, 1, 0), 1024, "unsupported mix"),
+    ((1, 0, 1, 0), 0, "count outside"),
+    ((1, 0, 1, 0), 1 << 31, "count outside"),
+])
+def test_stream_probe_rejects_bad_arguments(mix, count, msg):
+    # every case fails before any device work
+    lib = g.library()
+    st = lib.gasloc_stream_probe(*mix, None, None, count, None, None)
+    assert st == g.gasloc.GASLOC_EINVAL
+    assert msg in g.gasloc.gasloc_last_error(None)
+
+
+def test_stream_probe_rejects_null_and_misaligned_streams():
+    lib = g.library()
+    src = (ctypes.c_void_p * 1)(None)
+    dst = (ctypes.c_void_p * 1)(0x1000)
+    assert lib.gasloc_stream_probe(1, 0, 1, 0, src, dst, 64, None, None) == g.gasloc.GASLOC_EINVAL
+    assert "source" in g.gasloc.gasloc_last_error(None)
+    src = (ctypes.c_void_p * 1)(0x1008)
+    assert lib.gasloc_stream_probe(1, 0, 1, 0, src, dst, 64, None, None) == g.gasloc.GASLOC_EINVAL
+    assert "misaligned" in g.gasloc.gasloc_last_error(None)
+    src = (ctypes.c_void_p * 4)(0x1000, 0x2000, 0x3000, 0x4000)
+    assert lib.gasloc_stream_probe(4, 0, 0, 0, src, None, 64, None, None) == g.gasloc.GASLOC_EINVAL
+    assert "sink" in g.gasloc.gasloc_last_error(None)

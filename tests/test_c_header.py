@@ -1,4 +1,4 @@
-"""The C ABI from plain C (no GPU): include/gasloc.h compiles as C99 with
+"""The C ABI from plain C (no GPU): include/gasloc.h and gasloc_probe.h compile as C99 with
 warnings as errors, a C program links against libgasloc.so and its host-side
 calls agree with the oracle."""
 import os
@@ -40,6 +40,8 @@ def test_plain_c_consumer(tmp_path):
     f = lambda v: float(np.float32(v))  # the C program passes float arguments
     expect = [oracle.lr_schedule(f(1e-3), s, 100, f(0.1), f(0.01), 0.0) for s in (0, 10, 99)]
     assert [np.float32(v) for v in lr] == [np.float32(v) for v in expect]
+    assert lines["probe_mix"] == "1"    # GASLOC_EINVAL: unsupported mix of streams
+    assert lines["probe_count"] == "1"  # GASLOC_EINVAL: count outside [1, 2^31)
 
 
 @pytest.mark.gpu
