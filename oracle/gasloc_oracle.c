@@ -110,8 +110,8 @@ uint64_t orc_next(uint64_t *state) {
 }
 
 /* The generator state for communication round t: every worker derives the
- * same state from (seed, t), so all of them agree on the round's graph
- * ("a fresh permutation is sampled at every communication round", App. B.1). */
+ * same state from (seed, t), so all of them agree on the round's graph, which
+ * App. B.1 redraws for every communication round. */
 uint64_t orc_round_state(uint64_t seed, uint64_t t) { return orc_mix64(seed ^ orc_mix64(t)); }
 
 /* Uniform integer in [0, k): reject draws below 2^64 mod k, then reduce. */
@@ -368,8 +368,8 @@ int orc_topology_restricted(int kind, int n, int degree, uint64_t seed, uint64_t
   return ok ? nnz : -1;
 }
 
-/* Fault tolerance (section 3.2, "Fault tolerance": failed exchanges can be
- * skipped).  An exchange {i, j}, i != j, is skipped when worker i or j is
+/* Fault tolerance (section 3.2, paragraph "Fault tolerance": a round depends
+ * only on its activated exchanges, so one that fails may be dropped).  An exchange {i, j}, i != j, is skipped when worker i or j is
  * dead (alive[.] == 0) or the link failed (link_ok[i*n+j] == 0 or
  * link_ok[j*n+i] == 0); each endpoint then keeps for itself the weight it
  * would have given the other: W_ii += W_ij, W_ij = 0.  alive / link_ok may be
