@@ -127,8 +127,13 @@ int phase_blocks_per_cu(int dtype, bool fused, int form, const LaunchShape& shap
 int planned_blocks_per_cu(int dtype, bool fused, int form, const LaunchShape& shape, size_t dyn_lds);
 // Dynamic LDS bytes of one workgroup of the planned kernel (z slots only).
 size_t planned_lds_bytes(int slots, const LaunchShape& shape);
+// The standalone consensus error of columns [p_begin, p_end): one partial
+// per workgroup of kReduceThreads threads, each taking `per` consecutive
+// steps of 16-byte column groups; consensus_error_blocks gives the count.
+constexpr int kReduceThreads = 256;
+int consensus_error_blocks(int dtype, int64_t p_begin, int64_t p_end, int per);
 hipError_t launch_consensus_error(const void* x, int dtype, int64_t ld, int n, int64_t p_begin,
-                                  int64_t p_end, double* partials, int blocks, hipStream_t stream);
+                                  int64_t p_end, int per, double* partials, hipStream_t stream);
 hipError_t launch_finalize(const double* partials, int count, double* out, hipStream_t stream);
 // out[0] = sum of a[0..count), out[1] = sum of b[0..count), each as launch_finalize sums.
 hipError_t launch_finalize2(const double* a, const double* b, int count, double* out, hipStream_t stream);
@@ -140,8 +145,12 @@ constexpr int kFinalizeSegment = 4096;
 constexpr int kMaxPartials = 1 << 20;
 hipError_t launch_finalize2_large(const double* a, const double* b, int count, double* seg, double* out,
                                   hipStream_t stream);
-hipError_t launch_replica_mean(const void* x, int dtype, int64_t ld, int n, int64_t P, void* out,
-                               int blocks, hipStream_t stream);
+// *out = the sum of a[0..count), count <= kMaxPartials, in the same
+// segmented order (seg: at least ceil(count / kFinalizeSegment) doubles).
+hipError_t launch_finalize_large(const double* a, int count, double* seg, double* out, hipStream_t stream);
+// The network average of columns [0, P), workgroups as for the consensus error.
+hipError_t launch_replica_mean(const void* x, int dtype, int64_t ld, int n, int64_t P, int per, void* out,
+                               hipStream_t stream);
 
 // Dynamic LDS bytes one workgroup of the gossip kernel needs (z slots of
 // every thread plus the staged CSR); the kernel also uses kStaticLds bytes.

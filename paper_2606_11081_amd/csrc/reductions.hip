@@ -34,18 +34,21 @@ __device__ __forceinline__ void load_cols(const void* base, int64_t idx, int lo,
 // groups at the ends of the range are masked), with the loads of 8 workers
 // (fp32) or 4 (bf16, twice the columns; 8 left it register-bound) in
 // flight.  Per column the sums are those of the fused kernel: shifted by
-// worker 0's value, fp64, workers in order.
+// worker 0's value, fp64, workers in order.  Workgroup b takes the `per`
+// consecutive steps of blockDim.x groups starting at group b * per *
+// blockDim.x (tile order, as the round kernels) and writes one partial.
 template <int DT>
 __global__ __launch_bounds__(256) void k_consensus_error(const void* x, int64_t ld, int n,
-                                                         int64_t p_begin, int64_t p_end,
+                                                         int64_t p_begin, int64_t p_end, int per,
                                                          double* partials) {
   constexpr int V = DT == GASLOC_BF16 ? 8 : 4, R = DT == GASLOC_BF16 ? 4 : 8;
   const double inv_n = 1.0 / static_cast<double>(n);
   const int64_t base = p_begin - p_begin % V;
   const int64_t groups = (p_end - base + V - 1) / V;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  const int64_t g0 = static_cast<int64_t>(blockIdx.x) * per * blockDim.x;
+  const int64_t g_end = groups - g0 < static_cast<int64_t>(per) * blockDim.x ? groups : g0 + per * blockDim.x;
   double ce = 0.0;
-  for (int64_t gi = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; gi < groups; gi += stride) {
+  for (int64_t gi = g0 + threadIdx.x; gi < g_end; gi += blockDim.x) {
     const int64_t p = base + gi * V;
     const int lo = p < p_begin ? static_cast<int>(p_begin - p) : 0;
     const int hi = p_end - p < V ? static_cast<int>(p_end - p) : V;
@@ -110,9 +113,10 @@ __global__ __launch_bounds__(256) void k_finalize2(const double* a, const double
   }
 }
 
-// First level of launch_finalize2_large: workgroup s sums the partials
-// [s * kFinalizeSegment, (s + 1) * kFinalizeSegment) of both arrays (fewer in
-// the last segment) in k_finalize2's order, into seg[s] and seg[S + s].
+// First level of the segmented finalize: workgroup s sums the partials
+// [s * kFinalizeSegment, (s + 1) * kFinalizeSegment) of `a` (and of `b`
+// unless it is NULL; fewer in the last segment) in k_finalize's order, into
+// seg[s] (and seg[S + s]).
 __global__ __launch_bounds__(256) void k_finalize_segments(const double* a, const double* b, int count,
                                                            double* seg) {
   const int begin = blockIdx.x * kFinalizeSegment;
@@ -120,25 +124,27 @@ __global__ __launch_bounds__(256) void k_finalize_segments(const double* a, cons
   double va = 0.0, vb = 0.0;
   for (int k = begin + threadIdx.x; k < end; k += blockDim.x) {
     va += a[k];
-    vb += b[k];
+    if (b) vb += b[k];
   }
   double ta, tb;
   block_sum2(va, vb, ta, tb);
   if (threadIdx.x == 0) {
     seg[blockIdx.x] = ta;
-    seg[gridDim.x + blockIdx.x] = tb;
+    if (b) seg[gridDim.x + blockIdx.x] = tb;
   }
 }
 
 // a6: network average, fp64 sum in worker order, rounded to the param dtype;
-// 16 bytes of columns per thread, the loads of 8 workers in flight at a time.
+// 16 bytes of columns per thread, the loads of 8 workers in flight at a time;
+// workgroups in tile order, `per` steps each.
 template <int DT>
-__global__ __launch_bounds__(256) void k_replica_mean(const void* x, int64_t ld, int n, int64_t P,
+__global__ __launch_bounds__(256) void k_replica_mean(const void* x, int64_t ld, int n, int64_t P, int per,
                                                       void* out) {
   constexpr int V = DT == GASLOC_BF16 ? 8 : 4, R = 8;
   const int64_t groups = (P + V - 1) / V;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
-  for (int64_t gi = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; gi < groups; gi += stride) {
+  const int64_t g0 = static_cast<int64_t>(blockIdx.x) * per * blockDim.x;
+  const int64_t g_end = groups - g0 < static_cast<int64_t>(per) * blockDim.x ? groups : g0 + per * blockDim.x;
+  for (int64_t gi = g0 + threadIdx.x; gi < g_end; gi += blockDim.x) {
     const int64_t p = gi * V;
     const int cnt = static_cast<int>(P - p < V ? P - p : V);
     double s[V];
@@ -167,15 +173,34 @@ __global__ __launch_bounds__(256) void k_replica_mean(const void* x, int64_t ld,
 
 }  // namespace
 
+int consensus_error_blocks(int dtype, int64_t p_begin, int64_t p_end, int per) {
+  const int V = dtype == GASLOC_BF16 ? 8 : 4;
+  const int64_t base = p_begin - p_begin % V;
+  const int64_t groups = (p_end - base + V - 1) / V;
+  const int64_t span = static_cast<int64_t>(per) * kReduceThreads;
+  const int64_t blocks = (groups + span - 1) / span;
+  return static_cast<int>(blocks < 1 ? 1 : (blocks > (int64_t(1) << 30) ? (int64_t(1) << 30) : blocks));
+}
+
 hipError_t launch_consensus_error(const void* x, int dtype, int64_t ld, int n, int64_t p_begin,
-                                  int64_t p_end, double* partials, int blocks, hipStream_t stream) {
+                                  int64_t p_end, int per, double* partials, hipStream_t stream) {
+  const int blocks = consensus_error_blocks(dtype, p_begin, p_end, per);
   if (dtype == GASLOC_BF16)
-    hipLaunchKernelGGL((k_consensus_error<GASLOC_BF16>), dim3(blocks), dim3(256), 0, stream, x, ld, n,
-                       p_begin, p_end, partials);
+    hipLaunchKernelGGL((k_consensus_error<GASLOC_BF16>), dim3(blocks), dim3(kReduceThreads), 0, stream, x, ld,
+                       n, p_begin, p_end, per, partials);
   else
-    hipLaunchKernelGGL((k_consensus_error<GASLOC_F32>), dim3(blocks), dim3(256), 0, stream, x, ld, n,
-                       p_begin, p_end, partials);
+    hipLaunchKernelGGL((k_consensus_error<GASLOC_F32>), dim3(blocks), dim3(kReduceThreads), 0, stream, x, ld, n,
+                       p_begin, p_end, per, partials);
   return hipGetLastError();
+}
+
+hipError_t launch_finalize_large(const double* a, int count, double* seg, double* out, hipStream_t stream) {
+  if (count <= kFinalizeSegment) return launch_finalize(a, count, out, stream);
+  const int segments = (count + kFinalizeSegment - 1) / kFinalizeSegment;
+  hipLaunchKernelGGL(k_finalize_segments, dim3(segments), dim3(256), 0, stream, a, nullptr, count, seg);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_finalize(seg, segments, out, stream);
 }
 
 hipError_t launch_finalize(const double* partials, int count, double* out, hipStream_t stream) {
@@ -198,14 +223,15 @@ hipError_t launch_finalize2_large(const double* a, const double* b, int count, d
   return launch_finalize2(seg, seg + segments, segments, out, stream);
 }
 
-hipError_t launch_replica_mean(const void* x, int dtype, int64_t ld, int n, int64_t P, void* out,
-                               int blocks, hipStream_t stream) {
+hipError_t launch_replica_mean(const void* x, int dtype, int64_t ld, int n, int64_t P, int per, void* out,
+                               hipStream_t stream) {
+  const int blocks = consensus_error_blocks(dtype, 0, P, per);
   if (dtype == GASLOC_BF16)
-    hipLaunchKernelGGL((k_replica_mean<GASLOC_BF16>), dim3(blocks), dim3(256), 0, stream, x, ld, n, P,
-                       out);
+    hipLaunchKernelGGL((k_replica_mean<GASLOC_BF16>), dim3(blocks), dim3(kReduceThreads), 0, stream, x, ld, n, P,
+                       per, out);
   else
-    hipLaunchKernelGGL((k_replica_mean<GASLOC_F32>), dim3(blocks), dim3(256), 0, stream, x, ld, n, P,
-                       out);
+    hipLaunchKernelGGL((k_replica_mean<GASLOC_F32>), dim3(blocks), dim3(kReduceThreads), 0, stream, x, ld, n, P,
+                       per, out);
   return hipGetLastError();
 }
 

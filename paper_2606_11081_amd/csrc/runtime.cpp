@@ -89,7 +89,6 @@ struct gasloc_ctx {
   double* d_ce = nullptr;  // [2]: consensus error, squared pseudo-gradients of the last round
   double* h_ce = nullptr;  // [2] pinned
 
-  int reduce_blocks = 0;
   size_t lds_per_block_max = 0;
   size_t lds_per_cu = 0;
 
@@ -363,10 +362,21 @@ bool use_planned_kernel(const gasloc_ctx& c) {
   return c.n > 16;
 }
 
+// Steps of the standalone consensus error per workgroup: 8 (as the round
+// kernels), fewer on short ranges so that every CU still gets 16 workgroups.
+int reduce_per(const gasloc_ctx& c, int64_t p0, int64_t p1) {
+  const int V = c.hp.param_dtype == GASLOC_BF16 ? 8 : 4;
+  const int64_t steps = ((p1 - p0 + V) / V + gasloc::kReduceThreads - 1) / gasloc::kReduceThreads;
+  return static_cast<int>(std::min<int64_t>(8, std::max<int64_t>(1, steps / (16 * int64_t(c.cus)))));
+}
+
 gasloc_status reduce_cols(gasloc_ctx* c, int64_t p0, int64_t p1) {
-  HIP_TRY(c, gasloc::launch_consensus_error(c->buf.x, c->hp.param_dtype, c->buf.ld, c->n, p0, p1,
-                                            c->d_partials, c->reduce_blocks, c->stream));
-  HIP_TRY(c, gasloc::launch_finalize(c->d_partials, c->reduce_blocks, c->d_ce, c->stream));
+  const int per = reduce_per(*c, p0, p1);
+  const int blocks = gasloc::consensus_error_blocks(c->hp.param_dtype, p0, p1, per);
+  HIP_TRY(c, gasloc::launch_consensus_error(c->buf.x, c->hp.param_dtype, c->buf.ld, c->n, p0, p1, per,
+                                            c->d_partials, c->stream));
+  HIP_TRY(c, gasloc::launch_finalize_large(c->d_partials, blocks, c->d_partials + 2 * gasloc::kMaxPartials,
+                                           c->d_ce, c->stream));
   return GASLOC_OK;
 }
 
@@ -663,7 +673,6 @@ gasloc_status gasloc_init(int32_t n, int64_t P, const gasloc_topology* topology,
     release(c);
     return fail(nullptr, GASLOC_EINVAL, "gossip workgroup does not fit the device's LDS");
   }
-  c->reduce_blocks = c->cus * 4;
 
   if ((e = hipMalloc(&c->d_csr, stage_bytes(n))) != hipSuccess) return init_fail(e, "hipMalloc csr");
   if ((e = hipMalloc(&c->d_partials, sizeof(double) * kPartialWords)) != hipSuccess)
@@ -789,8 +798,8 @@ gasloc_status gasloc_replica_mean(gasloc_ctx* c, void* out) {
   if (c->failed) return fail(c, GASLOC_ESTATE, "context unusable after a device error: " + c->err);
   if (!out || !aligned16(out)) return fail(c, GASLOC_EINVAL, "out must be non-NULL and 16-byte aligned");
   DeviceGuard guard(c->device);
-  HIP_TRY(c, gasloc::launch_replica_mean(c->buf.x, c->hp.param_dtype, c->buf.ld, c->n, c->P, out,
-                                         c->reduce_blocks, c->stream));
+  HIP_TRY(c, gasloc::launch_replica_mean(c->buf.x, c->hp.param_dtype, c->buf.ld, c->n, c->P,
+                                         reduce_per(*c, 0, c->P), out, c->stream));
   return GASLOC_OK;
 }
 
