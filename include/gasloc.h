@@ -230,6 +230,29 @@ gasloc_status gasloc_pseudo_gradient_sq(gasloc_ctx *ctx, double *out);
 gasloc_status gasloc_consensus_error_cols(gasloc_ctx *ctx, int64_t p_begin, int64_t p_end,
                                           double *out);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * consensus error of gasloc_consensus_error_cols without a context.  x:
+ * device [n, ld] in param_dtype (gasloc_dtype), 16-byte aligned, ld *
+ * sizeof(param) a multiple of 16; columns [p_begin, p_end), 0 <= p_begin <=
+ * p_end <= ld, p_end < 2^31; out: device, one fp64, 8-byte aligned, written
+ * on hip_stream (the call does not wait).  Same per-column arithmetic as
+ * gasloc_consensus_error_cols; on ranges of at least 8 * 16 * 256 steps of
+ * 1024 fp32 (2048 bf16) columns per CU it groups the sums the same way too.
+ * Scratch: a fixed 512 KiB + 128 B device array inside the library (one copy
+ * per GPU, held until the process ends); the call allocates nothing and calls
+ * no allocating routine.  Limit: at most 2^16 workgroups of 8 x 256 column
+ * groups, i.e. 2^29 fp32 or 2^30 bf16 columns per call (EINVAL beyond; the
+ * error is additive over columns, so split the range and add the results).
+ * Nothing in the scratch has to start at zero (every partial is written
+ * before it is read).  Calls on one GPU share its scratch: calls that overlap
+ * in time on one GPU (different streams, or different host threads) race;
+ * calls in order on one stream do not.  Errors: EINVAL (checked before any
+ * device work), EDEVICE. */
+gasloc_status gasloc_consensus_error_cols_noalloc(const void *x, int32_t param_dtype, int32_t n, int64_t ld,
+                                                  int64_t p_begin, int64_t p_end, double *out,
+                                                  void *hip_stream);
+
 /* Network average xbar_p = (1/n) sum_i x_ip (Algorithm 1 output), summed in
  * fp64 in worker order and rounded to the param dtype, into out (device,
  * [P] of the param dtype, 16-byte aligned).  Enqueues one kernel. */

@@ -3,7 +3,19 @@
 // network average.
 #pragma clang fp contract(off)
 
+#include <mutex>
+#include <string>
+
 #include "device_common.h"
+
+// Scratch of gasloc_consensus_error_cols_noalloc: the workgroup partials, then
+// the finalize's segment sums.  A file-scope device array: every GPU the
+// library runs on holds its own copy for the life of the process.  In host
+// code `scratch` only names the symbol; its device address on the current GPU
+// comes from hipGetSymbolAddress (see noalloc_scratch below).
+constexpr int kNoAllocPartials = 1 << 16;
+constexpr int kNoAllocSegments = kNoAllocPartials / gasloc::kFinalizeSegment;
+static __device__ __align__(256) double scratch[kNoAllocPartials + kNoAllocSegments];
 
 namespace gasloc {
 namespace {
@@ -236,3 +248,62 @@ hipError_t launch_replica_mean(const void* x, int dtype, int64_t ld, int n, int6
 }
 
 }  // namespace gasloc
+
+namespace {
+
+constexpr int kNoAllocPer = 8;  // steps per workgroup, as the context's reduction on long ranges
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+double* g_scratch[kMaxDevices] = {};
+
+// Device address of `scratch` on the current GPU, looked up once per device
+// with that device current.
+hipError_t noalloc_scratch(double** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch[dev] = static_cast<double*>(p);
+  }
+  *out = g_scratch[dev];
+  return hipSuccess;
+}
+
+gasloc_status noalloc_fail(gasloc_status st, const std::string& msg) {
+  gasloc::set_thread_error("consensus_error_cols_noalloc: " + msg);
+  return st;
+}
+
+}  // namespace
+
+extern "C" gasloc_status gasloc_consensus_error_cols_noalloc(const void* x, int32_t param_dtype, int32_t n,
+                                                             int64_t ld, int64_t p_begin, int64_t p_end,
+                                                             double* out, void* hip_stream) {
+  if (!x || (reinterpret_cast<uintptr_t>(x) & 15u)) return noalloc_fail(GASLOC_EINVAL, "x must be non-NULL and 16-byte aligned");
+  if (!out || (reinterpret_cast<uintptr_t>(out) & 7u)) return noalloc_fail(GASLOC_EINVAL, "out must be non-NULL and 8-byte aligned");
+  if (param_dtype != GASLOC_F32 && param_dtype != GASLOC_BF16) return noalloc_fail(GASLOC_EINVAL, "param_dtype must be F32 or BF16");
+  if (n < 1 || n > gasloc::kMaxReplicas) return noalloc_fail(GASLOC_EINVAL, "n outside [1, 64]");
+  const int64_t elem = param_dtype == GASLOC_BF16 ? 2 : 4;
+  if (ld < 1 || (ld * elem) % 16 != 0) return noalloc_fail(GASLOC_EINVAL, "ld * sizeof(param) must be a positive multiple of 16 bytes");
+  if (p_begin < 0 || p_end < p_begin || p_end > ld || p_end >= (int64_t(1) << 31))
+    return noalloc_fail(GASLOC_EINVAL, "need 0 <= p_begin <= p_end <= ld and p_end < 2^31");
+  const int blocks = gasloc::consensus_error_blocks(param_dtype, p_begin, p_end, kNoAllocPer);
+  if (blocks > kNoAllocPartials) {
+    const int64_t most = int64_t(kNoAllocPartials) * kNoAllocPer * gasloc::kReduceThreads * (elem == 2 ? 8 : 4);
+    return noalloc_fail(GASLOC_EINVAL, "column range longer than the scratch allows (at most " + std::to_string(most) +
+                                           " columns of this dtype per call; split the range and add the results)");
+  }
+  double* ptr = nullptr;
+  hipError_t e = noalloc_scratch(&ptr);
+  if (e != hipSuccess) return noalloc_fail(GASLOC_EDEVICE, std::string("scratch address: ") + hipGetErrorString(e));
+  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  e = gasloc::launch_consensus_error(x, param_dtype, ld, n, p_begin, p_end, kNoAllocPer, ptr, stream);
+  if (e == hipSuccess) e = gasloc::launch_finalize_large(ptr, blocks, ptr + kNoAllocPartials, out, stream);
+  if (e != hipSuccess) return noalloc_fail(GASLOC_EDEVICE, hipGetErrorString(e));
+  return GASLOC_OK;
+}

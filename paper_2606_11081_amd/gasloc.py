@@ -71,6 +71,7 @@ _SIGNATURES = {
     "gasloc_consensus_error": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_double)]),
     "gasloc_pseudo_gradient_sq": (ctypes.c_int, [_vp, ctypes.POINTER(ctypes.c_double)]),
     "gasloc_consensus_error_cols": (ctypes.c_int, [_vp, _i64, _i64, ctypes.POINTER(ctypes.c_double)]),
+    "gasloc_consensus_error_cols_noalloc": (ctypes.c_int, [_vp, _i32, _i32, _i64, _i64, _i64, _vp, _vp]),
     "gasloc_replica_mean": (ctypes.c_int, [_vp, _vp]),
     "gasloc_topology_csr": (ctypes.c_int, [_vp, _u64, _vp, _vp, _vp, _i32, ctypes.POINTER(_i32)]),
     "gasloc_make_topology": (ctypes.c_int, [ctypes.POINTER(gasloc_topology), _i32, _u64, _vp, _vp, _vp,
@@ -220,6 +221,15 @@ def gasloc_consensus_error_cols(ctx, p_begin, p_end):
     out = ctypes.c_double()
     _check(library().gasloc_consensus_error_cols(ctx, int(p_begin), int(p_end), ctypes.byref(out)), ctx)
     return out.value
+
+
+def gasloc_consensus_error_cols_noalloc(x, param_dtype, n, ld, p_begin, p_end, out, stream=None):
+    """Context-free, allocation-free consensus error of columns [p_begin, p_end)
+    of the device buffer x ([n, ld]) into the device fp64 `out` (enqueued on
+    `stream`, a torch stream or None for the null stream; does not wait)."""
+    dt = GASLOC_BF16 if param_dtype in ("bf16", GASLOC_BF16) else GASLOC_F32
+    _check(library().gasloc_consensus_error_cols_noalloc(_dev(x), dt, int(n), int(ld), int(p_begin), int(p_end),
+                                                          _dev(out), None if stream is None else stream.cuda_stream))
 
 
 def gasloc_replica_mean(ctx, out):

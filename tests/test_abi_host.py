@@ -287,3 +287,34 @@ def test_stream_probe_rejects_null_and_misaligned_streams():
     src = (ctypes.c_void_p * 4)(0x1000, 0x2000, 0x3000, 0x4000)
     assert lib.gasloc_stream_probe(4, 0, 0, 0, src, None, 64, None, None) == g.gasloc.GASLOC_EINVAL
     assert "sink" in g.gasloc.gasloc_last_error(None)
+
+
+@pytest.mark.parametrize("args,msg", [
+    ((None, 0, 4, 1024, 0, 1024), "x must be"),
+    ((0x1008, 0, 4, 1024, 0, 1024), "x must be"),
+    ((0x1000, 2, 4, 1024, 0, 1024), "param_dtype"),
+    ((0x1000, 0, 0, 1024, 0, 1024), "n outside"),
+    ((0x1000, 0, 65, 1024, 0, 1024), "n outside"),
+    ((0x1000, 0, 4, 1026, 0, 1024), "multiple of 16"),
+    ((0x1000, 1, 4, 1028, 0, 1024), "multiple of 16"),
+    ((0x1000, 0, 4, 1024, 5, 4), "p_begin"),
+    ((0x1000, 0, 4, 1024, 0, 1028), "p_begin"),
+    ((0x1000, 0, 1, 1 << 31, 0, 1 << 31), "p_begin"),
+    # the scratch bound: 2^16 workgroups of 8 x 256 groups of 4 fp32 / 8 bf16 columns
+    ((0x1000, 0, 1, 1 << 30, 0, (1 << 29) + 1), "at most 536870912 columns"),
+    ((0x1000, 1, 1, 1 << 30, 4, (1 << 30) + 1), "p_begin"),
+    ((0x1000, 1, 1, (1 << 31) - 8, 0, (1 << 30) + 8), "at most 1073741824 columns"),
+])
+def test_noalloc_consensus_error_rejects_bad_arguments(args, msg):
+    # every case fails on the host, before the scratch lookup or any launch
+    out = 0x2000
+    st = g.library().gasloc_consensus_error_cols_noalloc(*args, out, None)
+    assert st == g.gasloc.GASLOC_EINVAL
+    assert msg in g.gasloc.gasloc_last_error(None)
+
+
+def test_noalloc_consensus_error_rejects_bad_output():
+    lib = g.library()
+    assert lib.gasloc_consensus_error_cols_noalloc(0x1000, 0, 4, 1024, 0, 1024, None, None) == g.gasloc.GASLOC_EINVAL
+    assert lib.gasloc_consensus_error_cols_noalloc(0x1000, 0, 4, 1024, 0, 1024, 0x2004, None) == g.gasloc.GASLOC_EINVAL
+    assert "out must be" in g.gasloc.gasloc_last_error(None)
