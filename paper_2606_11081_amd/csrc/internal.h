@@ -35,6 +35,10 @@ bool plan_round(int n, const int32_t* rp, const int32_t* col, const float* val, 
                 std::vector<int32_t>* ops, int* slots_used, std::string* err);
 bool verify_plan(int n, const int32_t* rp, const int32_t* col, const float* val, bool reuse_mix,
                  const int32_t* ops, int len, int slots, std::string* err);
+// The plan as the kernel reads it: every slot word (new values, each row's
+// own slot, each entry's slot) multiplied by `unit`, the byte stride between
+// a thread's slots in LDS.  For a plan verify_plan accepted.
+bool scale_plan_slots(std::vector<int32_t>* ops, int32_t unit, std::string* err);
 // Upper bound on the words of a plan for n workers.
 size_t plan_words_max(int n);
 bool skip_exchanges(int n, const int32_t* rp, const int32_t* col, const float* val, const uint8_t* alive,

@@ -23,6 +23,8 @@
 //   n_pre, n_rows, (worker, slot) x n_pre, row x n_rows,
 //   then per row: n_ent, own_slot, (slot, weight bits) x n_ent,
 //   or kPlanReuseMix, own_slot for a row that takes the last summed row's sum
+// The planner and its verifier use slot indices; scale_plan_slots turns them
+// into the byte offsets the kernel reads, for one launch shape.
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
@@ -234,6 +236,44 @@ bool plan_round(int n, const int32_t* rp, const int32_t* col, const float* val, 
     }
   }
   return verify_plan(n, rp, col, val, reuse_mix, ops->data(), static_cast<int>(ops->size()), *slots_used, err);
+}
+
+// Multiplies every slot word of a verified plan by `unit` (the launch's byte
+// stride between slots, so that the kernel adds a word to its own address
+// with no multiply): the slot of each new value, each row's own slot and the
+// slot of each entry.  Counts, worker and row indices and weights are kept.
+bool scale_plan_slots(std::vector<int32_t>* ops, int32_t unit, std::string* err) {
+  std::vector<int32_t>& o = *ops;
+  const int len = static_cast<int>(o.size());
+  if (len < 1 || o[0] < 1 || len < 1 + o[0] || unit < 1) {
+    *err = "round plan: cannot scale";
+    return false;
+  }
+  const int supers = o[0];
+  int64_t top = 0;
+  for (int s = 0; s < supers; ++s) {
+    int pc = o[1 + s];
+    const int npre = o[pc], nrows = o[pc + 1];
+    pc += 2;
+    for (int q = 0; q < npre; ++q, pc += 2) {
+      top = std::max<int64_t>(top, o[pc + 1]);
+      o[pc + 1] *= unit;
+    }
+    pc += nrows;
+    for (int q = 0; q < nrows; ++q) {
+      const int nent = o[pc];
+      top = std::max<int64_t>(top, o[pc + 1]);
+      o[pc + 1] *= unit;
+      pc += 2;
+      if (nent == kPlanReuseMix) continue;
+      for (int e = 0; e < nent; ++e, pc += 2) o[pc] *= unit;
+    }
+  }
+  if ((top + 1) * unit > (int64_t(1) << 30)) {
+    *err = "round plan: slot offsets out of range";
+    return false;
+  }
+  return true;
 }
 
 // Replays a plan symbolically: the start table points at consecutive

@@ -21,6 +21,9 @@
 //   npre, nrows, (worker, slot) x npre, row x nrows,
 //   then per row: nent, own_slot, (slot, weight bits) x nent, or
 //   kPlanReuseMix, own_slot (EQ, DAdam: the previous summed row's sum).
+// Slot words arrive as byte offsets (slot * threads * V * 4, scaled on the
+// host for the launch), so a slot's LDS address is one add to the thread's
+// own base.
 #pragma clang fp contract(off)
 
 #include "device_common.h"
@@ -170,10 +173,15 @@ struct CeSums {
   float mix[V];
 };
 
+// The value slot of this thread whose plan word (a byte offset) is `off`.
+__device__ __forceinline__ float* at_slot(float* mine, int32_t off) {
+  return reinterpret_cast<float*>(reinterpret_cast<char*>(mine) + off);
+}
+
 template <int DT, int V, int R, bool FUSED, int FORM, bool TAIL>
 __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* ops, int st, int64_t p,
                                                 int cnt_tail, const Staged<DT, V, R>& b, float* mine,
-                                                int slot_stride, CeSums<V>& cs) {
+                                                CeSums<V>& cs) {
   constexpr bool kEq = FORM == GASLOC_FORM_EQ;
   constexpr bool kAlg1 = FORM == GASLOC_FORM_ALG1;
   const int cnt = TAIL ? cnt_tail : V;
@@ -204,7 +212,7 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
     const int slot = ops[at + 3 + 2 * r];
     const int64_t e = static_cast<int64_t>(j) * a.ld + p;
     const bool stepped = (a.stepped >> j) & 1ull;
-    float* out = mine + slot * slot_stride;
+    float* out = at_slot(mine, slot);
     float xv[V], yv[V];
     if constexpr (kEq) {
       decode_raw<DT, V>(b.pa[r], xv);
@@ -272,7 +280,7 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
     const int64_t er = static_cast<int64_t>(row) * a.ld + p;
     float own[V];
     {
-      const float* zo = mine + ops[pos + 1] * slot_stride;
+      const float* zo = at_slot(mine, ops[pos + 1]);
 #pragma unroll
       for (int c = 0; c < V; ++c) own[c] = zo[c];
     }
@@ -300,7 +308,7 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
       float zk[4][V], wk[4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        const float* src = mine + ops[pos + 2 + 2 * t] * slot_stride;
+        const float* src = at_slot(mine, ops[pos + 2 + 2 * t]);
         wk[t] = __int_as_float(ops[pos + 3 + 2 * t]);
 #pragma unroll
         for (int c = 0; c < V; ++c) zk[t][c] = src[c];
@@ -316,7 +324,7 @@ __device__ __forceinline__ void planned_consume(const GossipArgs& a, plan_word* 
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           if (k0 + t >= count) break;
-          const float* src = mine + ops[pos + 2 + 2 * (k0 + t)] * slot_stride;
+          const float* src = at_slot(mine, ops[pos + 2 + 2 * (k0 + t)]);
           wk[t] = __int_as_float(ops[pos + 3 + 2 * (k0 + t)]);
 #pragma unroll
           for (int c = 0; c < V; ++c) zk[t][c] = src[c];
@@ -407,7 +415,6 @@ __global__ __launch_bounds__(256) void k_gossip_planned(GossipArgs a) {
   const int tid = threadIdx.x;
   const int steps = ops[0];
   const double inv_n = 1.0 / static_cast<double>(a.n);
-  const int slot_stride = nt * V;
   float* mine = zs + tid * V;
 
   // column groups (t0 + it) * nt + tid for the workgroup's steps it < iters
@@ -440,7 +447,7 @@ __global__ __launch_bounds__(256) void k_gossip_planned(GossipArgs a) {
     }
   };
   auto use = [&](const Staged<DT, V, R>& b) {
-    planned_consume<DT, V, R, FUSED, FORM, false>(a, ops, st_use, column(it_use), V, b, mine, slot_stride, cs);
+    planned_consume<DT, V, R, FUSED, FORM, false>(a, ops, st_use, column(it_use), V, b, mine, cs);
     if (++st_use == steps) {
 #pragma unroll
       for (int c = 0; c < V; ++c) ce += cs.q[c] - cs.s[c] * cs.s[c] * inv_n;
@@ -464,7 +471,7 @@ __global__ __launch_bounds__(256) void k_gossip_planned(GossipArgs a) {
     const int cnt = left >= V ? V : (left > 0 ? static_cast<int>(left) : 0);
     for (int st = 0; st < steps; ++st) {
       planned_issue<DT, V, R, FORM, true>(a, ops, st, col, cnt, A);
-      planned_consume<DT, V, R, FUSED, FORM, true>(a, ops, st, col, cnt, A, mine, slot_stride, cs);
+      planned_consume<DT, V, R, FUSED, FORM, true>(a, ops, st, col, cnt, A, mine, cs);
     }
 #pragma unroll
     for (int c = 0; c < V; ++c)

@@ -517,6 +517,12 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
   }
   tile_grid(*c, &shape);
   if (lds > c->lds_per_block_max) return fail(c, GASLOC_EINVAL, "gossip shape exceeds the device's LDS per workgroup");
+  if (planned) {  // slot words become byte offsets for this launch's shape
+    std::string err;
+    if (!gasloc::scale_plan_slots(&c->plan_ops, shape.threads * shape.vec * static_cast<int32_t>(sizeof(float)),
+                                  &err))
+      return fail(c, GASLOC_EINVAL, err);
+  }
   gasloc_status st = planned ? upload_plan(c, c->plan_ops) : upload_csr(c, rp, col, val, nnz);
   if (st != GASLOC_OK) return st;
 

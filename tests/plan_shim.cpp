@@ -34,6 +34,15 @@ int plan_shim_verify(int n, const int32_t* rp, const int32_t* col, const float* 
   return gasloc::verify_plan(n, rp, col, val, reuse_mix != 0, ops, len, slots, &e) ? 1 : 0;
 }
 
+// Scales the slot words of a plan in place (scale_plan_slots); 1 on success.
+int plan_shim_scale(int32_t* ops, int len, int32_t unit) {
+  std::vector<int32_t> v(ops, ops + len);
+  std::string e;
+  if (!gasloc::scale_plan_slots(&v, unit, &e)) return 0;
+  std::memcpy(ops, v.data(), v.size() * sizeof(int32_t));
+  return 1;
+}
+
 int plan_shim_reuse_code() { return gasloc::kPlanReuseMix; }
 
 int64_t plan_shim_words_max(int n) { return static_cast<int64_t>(gasloc::plan_words_max(n)); }

@@ -43,6 +43,7 @@ def shim(tmp_path_factory):
     lib.plan_shim_verify.argtypes = [ctypes.c_int, P(ctypes.c_int32), P(ctypes.c_int32), P(ctypes.c_float),
                                      ctypes.c_int, P(ctypes.c_int32), ctypes.c_int, ctypes.c_int]
     lib.plan_shim_words_max.restype = ctypes.c_int64
+    lib.plan_shim_scale.argtypes = [P(ctypes.c_int32), ctypes.c_int, ctypes.c_int32]
     return lib
 
 
@@ -242,3 +243,63 @@ def test_reused_sum_needs_equal_entries(shim):
         other[k] = np.nextafter(other[k], np.float32(1.0))
         assert not verify(shim, n, rp, col, other, ops, slots, True), r
 
+
+
+def slot_word_positions(ops):
+    """Indices of the words of a plan that name a slot, read off the encoding
+    independently of the library: each new value's slot, each row's own slot
+    and each entry's slot."""
+    reuse_code = -1
+    pos = []
+    S = int(ops[0])
+    for s in range(S):
+        pc = int(ops[1 + s])
+        npre, nrows = int(ops[pc]), int(ops[pc + 1])
+        pc += 2
+        for _ in range(npre):
+            pos.append(pc + 1)
+            pc += 2
+        pc += nrows
+        for _ in range(nrows):
+            nent = int(ops[pc])
+            pos.append(pc + 1)
+            pc += 2
+            if nent == reuse_code:
+                continue
+            for _ in range(nent):
+                pos.append(pc)
+                pc += 2
+    return pos
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("unit", [1, 4 * 64, 4 * 256 * 2, 4 * 256 * 4])
+def test_scaled_plans_hold_byte_offsets_of_the_same_slots(shim, kind, unit):
+    # the kernel reads slot words as byte offsets (slot * threads * V * 4):
+    # scaling multiplies exactly those words, and dividing them back gives a
+    # plan that replays bit for bit like the original
+    assert shim.plan_shim_reuse_code() == -1
+    n = 32
+    for t in range(3):
+        rp, col, val = oracle.topology_csr(kind, n, 3, t, 3)
+        for reuse in (False, True):
+            ops, slots = plan(shim, n, rp, col, val, reuse)
+            scaled = np.ascontiguousarray(ops.copy(), np.int32)
+            assert shim.plan_shim_scale(_ptr(scaled, ctypes.c_int32), len(scaled), unit) == 1
+            pos = slot_word_positions(ops)
+            other = np.setdiff1d(np.arange(len(ops)), pos)
+            assert np.array_equal(scaled[other], ops[other])
+            assert np.array_equal(scaled[pos], ops[pos] * unit)
+            back = scaled.copy()
+            back[pos] //= unit
+            z = np.random.default_rng(t).standard_normal(n).astype(np.float32)
+            got, _ = replay(shim, n, rp, col, val, back, slots, z, reuse)
+            assert np.array_equal(got.view(np.uint32), dense_order_sums(n, rp, col, val, z).view(np.uint32))
+
+
+def test_scaling_rejects_offsets_beyond_range(shim):
+    rp, col, val = oracle.topology_csr("complete", 64, 0, 0)
+    ops, slots = plan(shim, 64, rp, col, val, False)
+    assert slots == 64
+    big = np.ascontiguousarray(ops.copy(), np.int32)
+    assert shim.plan_shim_scale(_ptr(big, ctypes.c_int32), len(big), 1 << 25) == 0
