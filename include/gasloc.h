@@ -59,7 +59,14 @@ typedef enum {
 /* Communication graph of a round, W = I - alpha * Lambda (section 3.1).
  * Every neighbourhood contains the worker itself (section 3.1, Notation);
  * neighbourhoods are sets, and unless stated the weights are 1/|N_i|
- * (Algorithm 1's average over N_i).  Columns are ascending within a row. */
+ * (Algorithm 1's average over N_i).  Columns are ascending within a row.
+ * Cost: every graph gives the same results at any n, but beyond 16 workers
+ * the round keeps each column's live values in LDS, so graphs that need many
+ * of them at once run well below the HBM rate: the complete graph (all n
+ * live; rows share one sum) and the static exponential graph (28 to 64
+ * live) at n = 32-64 ran at 31-58% of peak bandwidth, the sparse 1-Peer,
+ * 2-Peer, ring and random 3-regular graphs at 69-77%.  Use dense graphs beyond
+ * 16 workers for checks (the complete graph is DiLoCo), not for speed. */
 typedef enum {
   GASLOC_TOPO_EXPLICIT = 0,       /* the caller passes W to every round            */
   GASLOC_TOPO_RING = 1,           /* static cycle {i-1, i, i+1} (Tables 1-3 "ring")  */
