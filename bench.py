@@ -35,6 +35,9 @@ PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, AMD specification
 INFINITY_CACHE_BYTES = 256e6  # MI355X last-level cache
 METRIC = "replica-param updates/s per gossip round; achieved HBM GB/s vs peak"
 DEFAULT_WORKLOAD = "onepeer-exp-n16-p350m"
+# the benchmark's five configurations by name
+CONFIGS = {"C1": "ring-n4-p1m", "C2": "exp-n8-p124m", "C3": "onepeer-exp-n16-p350m",
+           "C4": "regular3-n32-p150m-bf16", "C5": "matching-n64-p50m-hetH"}
 
 
 def log(msg):
@@ -137,9 +140,10 @@ def traffic_source(kernel, workload, n):
                       "counter of the streaming probe's copy of known size (in that profile's process)"}
 
 
-def _oracle_sample(w, columns, form, seed):
+def _oracle_sample(w, columns, form, seed, topo_seed=0):
     """An oracle on `columns` columns of the workload, with its x0 and one
-    gradient batch (host arrays, made before any timing)."""
+    gradient batch (host arrays, made before any timing); topo_seed is added
+    to the schedule's seed, as the benchmark's --seed does."""
     import numpy as np
 
     import gasloc_inputs as gi
@@ -148,7 +152,7 @@ def _oracle_sample(w, columns, form, seed):
     hp = oracle.OracleHParams(beta1=gi.BETA1, beta2=gi.BETA2, eps=gi.EPS, weight_decay=gi.WEIGHT_DECAY,
                               outer_lr=gi.OUTER_LR, outer_momentum=gi.OUTER_MOMENTUM,
                               nesterov=True, consensus_momentum=w.gamma if form == "eq" else 0.0, form=form)
-    o = oracle.Oracle(w.n, columns, hp, topology=w.topology, seed=gi.SEED_TOPOLOGY, degree=w.degree,
+    o = oracle.Oracle(w.n, columns, hp, topology=w.topology, seed=gi.SEED_TOPOLOGY + topo_seed, degree=w.degree,
                       precision="f32", param_dtype=w.param_dtype)
     rng = np.random.default_rng(seed)
     o.set_params((rng.standard_normal(columns) * 0.02).astype(np.float32))
@@ -169,11 +173,11 @@ def _oracle_round(o, g, H_i):
     o.consensus_error()
 
 
-def cpu_baseline(w, H_i, columns, form="eq"):
+def cpu_baseline(w, H_i, columns, form="eq", topo_seed=0):
     """The oracle as it stands, single-threaded, on `columns` columns of the
     same workload: one full round (all local steps, gossip, consensus error)
     in the same round form."""
-    o, g = _oracle_sample(w, columns, form, 0)
+    o, g = _oracle_sample(w, columns, form, 0, topo_seed)
     t0 = time.perf_counter()
     _oracle_round(o, g, H_i)
     dt = time.perf_counter() - t0
@@ -197,7 +201,7 @@ def host_threads():
     return max(1, t)
 
 
-def cpu_baseline_parallel(w, H_i, columns, form="eq", threads=None):
+def cpu_baseline_parallel(w, H_i, columns, form="eq", threads=None, topo_seed=0):
     """The same oracle on all host threads: the sample's columns split into
     one contiguous slice per thread, each slice an oracle of its own (every
     stored value depends only on its own column, so the slices are
@@ -207,7 +211,7 @@ def cpu_baseline_parallel(w, H_i, columns, form="eq", threads=None):
     threads = threads or host_threads()
     threads = max(1, min(threads, columns))
     bounds = [columns * k // threads for k in range(threads + 1)]
-    parts = [_oracle_sample(w, bounds[k + 1] - bounds[k], form, 100 + k) for k in range(threads)]
+    parts = [_oracle_sample(w, bounds[k + 1] - bounds[k], form, 100 + k, topo_seed) for k in range(threads)]
     start = threading.Barrier(threads + 1)
     errors = []
 
@@ -321,10 +325,11 @@ def stream_probe(names, dev, reps=5):
     return out
 
 
-def run_workload(w, form, steps, warmup, fuse, dev, log_prefix="bench"):
+def run_workload(w, form, steps, warmup, fuse, dev, log_prefix="bench", seed=0):
     """Whole rounds of one workload on the GPU: `warmup` untimed rounds, then
-    `steps` timed rounds, then 5 standalone gossip rounds.  Returns the
-    measurements; frees the workload's buffers before returning."""
+    `steps` timed rounds, then 5 standalone gossip rounds.  `seed` shifts the
+    schedule's seed and picks the gradient batch.  Returns the measurements;
+    frees the workload's buffers before returning."""
     import numpy as np
     import torch
 
@@ -338,13 +343,13 @@ def run_workload(w, form, steps, warmup, fuse, dev, log_prefix="bench"):
     log("%s: %s%s  (n=%d P=%d %s H=%s gamma=%g)" % (log_prefix, w.name, "" if form == "eq" else " " + form, w.n,
                                                    w.P, w.param_dtype,
                                                    "U{%d..%d}" % w.hetero_H if w.hetero_H else w.H, gamma))
-    lib = g.GASLoC(w.n, w.P, topology=w.topology, seed=gi.SEED_TOPOLOGY, degree=w.degree,
+    lib = g.GASLoC(w.n, w.P, topology=w.topology, seed=gi.SEED_TOPOLOGY + seed, degree=w.degree,
                    param_dtype=w.param_dtype, beta1=gi.BETA1, beta2=gi.BETA2, eps=gi.EPS,
                    weight_decay=gi.WEIGHT_DECAY, outer_lr=gi.OUTER_LR, outer_momentum=gi.OUTER_MOMENTUM,
                    outer_nesterov=True, consensus_momentum=gamma, round_form=form)
     lib.set_params(gi.make_x0(w.P, device=dev))
     grads = torch.empty((w.n, lib.ld), dtype=torch.float32, device=dev)
-    gi.fill_grads(grads, gi.worker_means(w.n), 0)
+    gi.fill_grads(grads, gi.worker_means(w.n), seed)
     stream = lib.stream
     torch.cuda.synchronize()
 
@@ -425,6 +430,16 @@ def run_workload(w, form, steps, warmup, fuse, dev, log_prefix="bench"):
     }
 
 
+def build_record():
+    """The loaded library's build record and whether its sources are this tree's."""
+    import paper_2606_11081_amd as g
+    from paper_2606_11081_amd import build as lib_build
+
+    info = g.gasloc.gasloc_build_info()
+    sha = lib_build.sources_sha()
+    return {"library": info, "tree_sources_sha": sha, "matches_tree": info.startswith("sources %s;" % sha)}
+
+
 def frac(x, ref):
     return round(x / ref, 4) if ref else None
 
@@ -463,6 +478,10 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--config", choices=sorted(CONFIGS), help="the workload by its configuration name (C1..C5)")
+    ap.add_argument("--rounds", type=int, default=None, help="the same as --steps")
+    ap.add_argument("--seed", type=int, default=0,
+                    help="added to the schedule's seed; also selects the gradient batch (default 0)")
     ap.add_argument("--workloads", default="auto",
                     help="other workloads timed after the headline one: 'auto' (all the others when the headline is "
                          "the default workload in the EQ form, else none), 'none', or a comma-separated list")
@@ -478,6 +497,10 @@ def main():
     args = ap.parse_args()
     if args.form in ("dadam", "local_dadam"):
         args.fuse = False
+    if args.config:
+        args.workload = CONFIGS[args.config]
+    if args.rounds is not None:
+        args.steps = args.rounds
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: every replica of the round lives on a single MI355X; "
@@ -494,7 +517,7 @@ def main():
     wname = w.name if args.form == "eq" else "%s-%s" % (w.name, args.form)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    r = run_workload(w, args.form, args.steps, args.warmup, args.fuse, dev)
+    r = run_workload(w, args.form, args.steps, args.warmup, args.fuse, dev, seed=args.seed)
     gamma, H_i = r["gamma"], r["H_i"]
     probe = {}
     if args.probe:
@@ -533,18 +556,21 @@ def main():
                    "local_steps": "U{%d..%d}" % w.hetero_H if w.hetero_H else w.H,
                    "gamma": gamma, "param_dtype": w.param_dtype, "state_dtype": "f32",
                    "last_local_step_fused": bool(args.fuse),
-                   "gradients": "one resident [n, ld] fp32 batch, drawn once (seed 2), read by every local step"},
+                   "seed": args.seed,
+                   "gradients": "one resident [n, ld] fp32 batch, drawn once (seed %d), read by every local step"
+                                % (gi.SEED_GRAD_BASE + args.seed)},
         "roofline": roofline,
     }
     out.update(recs)
     out["stream_probe"] = probe
+    out["build"] = build_record()
     out["consensus_error_last"] = r["ces"][-1]
     if not args.no_cpu_baseline:
         columns = min(args.cpu_columns, w.P) if args.cpu_columns > 0 else cpu_sample_columns(w, H_i)
         log("bench: timing the oracle on %d columns" % columns)
-        out["cpu_baseline"] = cpu_baseline(w, H_i, columns, args.form)
+        out["cpu_baseline"] = cpu_baseline(w, H_i, columns, args.form, args.seed)
         log("bench: timing the oracle on %d host threads" % host_threads())
-        out["cpu_baseline_all_threads"] = cpu_baseline_parallel(w, H_i, columns, args.form)
+        out["cpu_baseline_all_threads"] = cpu_baseline_parallel(w, H_i, columns, args.form, topo_seed=args.seed)
 
     if args.workloads == "auto":
         others = [k for k in gi.WORKLOADS if k != w.name] if (w.name == DEFAULT_WORKLOAD and args.form == "eq") else []
@@ -556,7 +582,7 @@ def main():
         out["workloads"] = {}
     for name in others:
         wo = gi.WORKLOADS[name]
-        ro = run_workload(wo, "eq", args.workload_steps, 2, True, dev, log_prefix="bench (workloads)")
+        ro = run_workload(wo, "eq", args.workload_steps, 2, True, dev, log_prefix="bench (workloads)", seed=args.seed)
         po = {}
         # a workload whose round fits the 256 MB Infinity Cache is not an HBM
         # stream: no probe fraction for it
@@ -572,8 +598,8 @@ def main():
             Hw = ro["H_i"]
             columns = max(1, cpu_sample_columns(wo, Hw) // 3)  # about 4 s of single-core work
             log("bench (workloads): timing the oracle on %d columns of %s" % (columns, name))
-            rec["cpu_baseline"] = cpu_baseline(wo, Hw, columns)
-            rec["cpu_baseline_all_threads"] = cpu_baseline_parallel(wo, Hw, columns)
+            rec["cpu_baseline"] = cpu_baseline(wo, Hw, columns, topo_seed=args.seed)
+            rec["cpu_baseline_all_threads"] = cpu_baseline_parallel(wo, Hw, columns, topo_seed=args.seed)
         out["workloads"][name] = rec
     print(json.dumps(out), flush=True)
 

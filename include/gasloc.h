@@ -319,6 +319,13 @@ gasloc_status gasloc_set_counters(gasloc_ctx *ctx, const int64_t *k, const uint8
  * failing context-free call (or gasloc_init) on this thread. */
 const char *gasloc_last_error(const gasloc_ctx *ctx);
 
+/* How this library was built: "sources <16 hex digits>; <arch>; <flags>",
+ * the hex digits being the start of a SHA-256 over the source files it was
+ * compiled from (paper_2606_11081_amd/build.py, sources_sha), so that a
+ * caller can tell whether a prebuilt library matches a source tree.  A
+ * static string; never NULL. */
+const char *gasloc_build_info(void);
+
 /* Wait for the context's stream, free its scratch; the caller's buffers are
  * untouched.  NULL is ignored. */
 void gasloc_destroy(gasloc_ctx *ctx);

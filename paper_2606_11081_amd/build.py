@@ -7,6 +7,7 @@ instructions disabled (a gfx950 target feature), then the host pass, which
 embeds the device binary and is not given that feature (the host target does
 not know it).
 """
+import hashlib
 import os
 import subprocess
 import sys
@@ -32,6 +33,24 @@ HOST_CXX = [os.path.join(ROCM, "llvm", "bin", "clang++"), "-D__HIP_PLATFORM_AMD_
             "-I", os.path.join(ROCM, "include")]
 
 
+def sources_sha():
+    """SHA-256 (first 16 hex digits) of every source the library is compiled
+    from: csrc/ and include/, files in name order, each name then its bytes."""
+    h = hashlib.sha256()
+    for d in (CSRC, os.path.join(ROOT, "include")):
+        for name in sorted(os.listdir(d)):
+            if name.endswith((".hip", ".cpp", ".h")):
+                h.update(name.encode())
+                with open(os.path.join(d, name), "rb") as f:
+                    h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def build_info():
+    """What gasloc_build_info() of a library built now returns."""
+    return "sources %s; %s; -O3 -ffp-contract=off; device pass without packed-fp32" % (sources_sha(), ARCH)
+
+
 def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -43,9 +62,11 @@ def device_binary(src):
     return os.path.join(BUILD, os.path.splitext(src)[0] + ".hipfb")
 
 
-def _compile(src, verbose):
+def _compile(src, verbose, info):
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
     path = os.path.join(CSRC, src)
+    if src == "runtime.cpp":
+        return _run(HOST_CXX + COMMON + ['-DGASLOC_BUILD_INFO="%s"' % info, "-c", path, "-o", obj], verbose) or obj
     if src.endswith(".hip"):
         fatbin = device_binary(src)
         _run(["hipcc"] + COMMON + HIP + DEVICE_ONLY + ["-c", path, "-o", fatbin], verbose)
@@ -58,8 +79,9 @@ def _compile(src, verbose):
 
 def build(verbose=False):
     os.makedirs(BUILD, exist_ok=True)
+    info = build_info()
     with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
+        objs = list(ex.map(lambda s: _compile(s, verbose, info), SOURCES))
     tmp = LIB + ".tmp"
     _run(["hipcc", "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs, verbose)
     os.replace(tmp, LIB)

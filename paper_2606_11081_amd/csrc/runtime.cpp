@@ -887,6 +887,11 @@ gasloc_status gasloc_set_counters(gasloc_ctx* c, const int64_t* k, const uint8_t
 
 const char* gasloc_last_error(const gasloc_ctx* c) { return c ? c->err.c_str() : g_thread_error.c_str(); }
 
+#ifndef GASLOC_BUILD_INFO
+#define GASLOC_BUILD_INFO "sources unknown"
+#endif
+const char* gasloc_build_info(void) { return GASLOC_BUILD_INFO; }
+
 void gasloc_destroy(gasloc_ctx* c) {
   if (!c) return;
   DeviceGuard guard(c->device);

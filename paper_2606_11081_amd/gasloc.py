@@ -86,6 +86,7 @@ _SIGNATURES = {
                                             ctypes.c_float]),
     "gasloc_stream_probe": (ctypes.c_int, [_i32, _i32, _i32, _i32, _vp, _vp, _i64, _vp, _vp]),
     "gasloc_last_error": (ctypes.c_char_p, [_vp]),
+    "gasloc_build_info": (ctypes.c_char_p, []),
     "gasloc_destroy": (None, [_vp]),
 }
 
@@ -321,6 +322,11 @@ def gasloc_stream_probe(reads_f32, reads_bf16, writes_f32, writes_bf16, src, dst
 def gasloc_last_error(ctx=None):
     msg = library().gasloc_last_error(ctx)
     return msg.decode() if msg else ""
+
+
+def gasloc_build_info():
+    """The library's build record: the hash of the sources it was compiled from, arch, flags."""
+    return library().gasloc_build_info().decode()
 
 
 def gasloc_destroy(ctx):

@@ -318,3 +318,13 @@ def test_noalloc_consensus_error_rejects_bad_output():
     assert lib.gasloc_consensus_error_cols_noalloc(0x1000, 0, 4, 1024, 0, 1024, None, None) == g.gasloc.GASLOC_EINVAL
     assert lib.gasloc_consensus_error_cols_noalloc(0x1000, 0, 4, 1024, 0, 1024, 0x2004, None) == g.gasloc.GASLOC_EINVAL
     assert "out must be" in g.gasloc.gasloc_last_error(None)
+
+
+def test_library_was_built_from_this_tree():
+    # gasloc_build_info carries the hash of the sources the library was
+    # compiled from; a library left over from other sources fails here
+    from paper_2606_11081_amd import build as lib_build
+
+    info = g.gasloc.gasloc_build_info()
+    assert info == lib_build.build_info(), (info, lib_build.build_info())
+    assert "gfx950" in info and "packed-fp32" in info

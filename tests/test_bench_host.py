@@ -238,3 +238,22 @@ def test_scripts_use_no_unbound_names():
         unbound = sorted({n.id for n in ast.walk(tree) if isinstance(n, ast.Name) and isinstance(n.ctx, ast.Load)}
                          - bound)
         assert not unbound, (script, unbound)
+
+
+def test_configurations_name_the_workloads(bench):
+    assert set(bench.CONFIGS.values()) == set(gi.WORKLOADS)
+    assert bench.CONFIGS["C3"] == bench.DEFAULT_WORKLOAD
+    for name, wl in bench.CONFIGS.items():
+        w = gi.WORKLOADS[wl]
+        assert (name, w.n) in {("C1", 4), ("C2", 8), ("C3", 16), ("C4", 32), ("C5", 64)}
+
+
+def test_probe_mixes_match_the_kernel_bytes(bench):
+    # every kernel's probe mix moves that kernel's bytes per element (EQ form)
+    for wl in gi.WORKLOADS.values():
+        sp = bench.param_bytes(wl.param_dtype)
+        mixes = bench.kernel_mixes(wl.param_dtype, wl.gamma)
+        per = lambda m: bench.probe_mix_bytes(bench.PROBE_MIXES[m], 1)  # noqa: E731
+        assert per(mixes["adamw"]) == bench.adamw_bytes_per_rp(sp)
+        assert per(mixes["round"]) == bench.gossip_bytes_per_rp(sp, wl.gamma)
+        assert per(mixes["fused"]) == bench.fused_bytes_per_rp(sp, wl.gamma, True, True)
