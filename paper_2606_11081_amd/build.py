@@ -18,8 +18,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libgasloc.so")
-SOURCES = ["adamw.hip", "round_phase.hip", "round_planned.hip", "reductions.hip", "stream_probe.hip", "runtime.cpp",
-           "topology.cpp", "schedule.cpp", "plan.cpp"]
+SOURCES = ["adamw.hip", "round_phase.hip", "round_planned.hip", "round_shared.hip", "reductions.hip",
+           "stream_probe.hip", "runtime.cpp", "topology.cpp", "schedule.cpp", "plan.cpp"]
 ARCH = "gfx950"
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-ffp-contract=off",

@@ -96,6 +96,11 @@ struct GossipArgs {
   const int32_t* ops;
   int32_t slots;
 
+  // rows that all hold the same entries (k_gossip_shared only): bit j of
+  // shared_mask says column j is an entry, with weight shared_w[j]
+  uint64_t shared_mask;
+  float shared_w[kMaxReplicas];
+
   // Fused last local step (the fused kernel only): every worker i with bit i
   // of `active` first takes one AdamW step from its live iterate; the new
   // iterate feeds delta directly and is never written back (it is logically
@@ -124,6 +129,11 @@ hipError_t launch_gossip_round(const GossipArgs& a, int dtype, bool fused, int f
                                const LaunchShape& shape, hipStream_t stream);
 hipError_t launch_gossip_planned(const GossipArgs& a, int dtype, bool fused, int form, const LaunchShape& shape,
                                  hipStream_t stream);
+// Rounds whose rows all hold the same entries, EQ form (round_shared.hip):
+// shape.vec must be shared_vec(n, dtype); no dynamic LDS.
+int shared_vec(int n, int dtype);
+hipError_t launch_gossip_shared(const GossipArgs& a, int dtype, bool fused, const LaunchShape& shape,
+                                hipStream_t stream);
 // Workgroups of the selected phase or planned round kernel that one CU
 // holds at once, given its registers, LDS and wave limits (0 if the query
 // fails).

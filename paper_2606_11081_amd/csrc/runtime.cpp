@@ -345,21 +345,50 @@ gasloc_status upload_plan(gasloc_ctx* c, const std::vector<int32_t>& ops) {
 
 // Which kernel runs a round: the phase kernel keeps every worker's slot
 // value in LDS; the planned kernel (plan.cpp) keeps only the live ones and
-// lets rows with equal entries share one neighbour sum.  Measured on MI355X
-// (EQ form, gossip round alone): beyond 16 workers planned is faster on every
-// graph (n=64: 1-Peer 15.0 vs 28.2 ms, complete 34.5 vs 247 ms; n=32:
-// 3-regular 1.9x, complete 28.8 vs 74.8 ms) or tied (n=64 exponential); at
-// n <= 16 the phase kernel keeps more loads in flight and the two tie, except
-// the fused round (n=16 one-peer exponential: 44.8 vs 45.4 ms) and the
-// complete graph (n=16: 29.8 vs 26.1 ms).
+// lets rows with equal entries share one neighbour sum; the shared kernel
+// serves rounds whose rows all hold the same entries (the complete graph) in
+// the EQ form, with one running sum per column and each row's own term in
+// registers.  Measured on MI355X (EQ form, gossip round alone): beyond
+// 16 workers planned is faster than phase on every graph (n=64: 1-Peer 15.0 vs
+// 28.2 ms, complete 34.5 vs 247 ms; n=32: 3-regular 1.9x, complete 28.8 vs
+// 74.8 ms) or tied (n=64 exponential); at n <= 16 the phase kernel keeps more
+// loads in flight and the two tie, except the fused round (n=16 one-peer
+// exponential: 44.8 vs 45.4 ms) and the complete graph (n=16: 29.8 vs 26.1 ms).
+enum class RoundKernel { kPhase, kPlanned, kShared };
+
+// True if every row of W holds the entries of row 0 (columns and weight bits).
+bool rows_all_equal(int n, const int32_t* rp, const int32_t* col, const float* val) {
+  const int32_t len = rp[1] - rp[0];
+  for (int i = 1; i < n; ++i) {
+    if (rp[i + 1] - rp[i] != len) return false;
+    if (std::memcmp(col + rp[i], col + rp[0], sizeof(int32_t) * static_cast<size_t>(len)) != 0 ||
+        std::memcmp(val + rp[i], val + rp[0], sizeof(float) * static_cast<size_t>(len)) != 0)
+      return false;
+  }
+  return true;
+}
+
+// The shared kernel on the complete graph (EQ, gamma = 0.1, round alone /
+// fused last step + round, against the kernel used before it): fp32 n=16,
+// P=350M 25.3-25.7 / 44.3-44.4 ms (planned 25.9-26.0 / 44.3-44.4); n=32,
+// P=150M 23.0 / 40.8 ms (planned 28.6 / 45.7); n=64, P=50M 17.8 / 34.1 ms
+// (planned 34.8 / 56.6); bf16 n=16 20.6 / 40.9 ms (phase 35.1 / 46.3); n=32
+// 23.6 / 46.6 ms (planned 30.9 / 44.6); n=64 22.0 / 34.4 ms (planned 38.1 /
+// 55.9).  So it serves every such round except the fused bf16 one at 17-32
+// workers.
+//
 // Test hook (documented in gasloc.h): GASLOC_GOSSIP_KERNEL=phase|planned forces
 // one kernel, so that the test suite can run every case through both.
-bool use_planned_kernel(const gasloc_ctx& c) {
+RoundKernel pick_round_kernel(const gasloc_ctx& c, const int32_t* rp, const int32_t* col, const float* val,
+                              bool fused) {
   if (const char* env = std::getenv("GASLOC_GOSSIP_KERNEL")) {
-    if (std::strcmp(env, "phase") == 0) return false;
-    if (std::strcmp(env, "planned") == 0) return true;
+    if (std::strcmp(env, "phase") == 0) return RoundKernel::kPhase;
+    if (std::strcmp(env, "planned") == 0) return RoundKernel::kPlanned;
   }
-  return c.n > 16;
+  const bool fused_bf16_17_32 = fused && c.hp.param_dtype == GASLOC_BF16 && c.n > 16 && c.n <= 32;
+  if (c.hp.round_form == GASLOC_FORM_EQ && !fused_bf16_17_32 && rows_all_equal(c.n, rp, col, val))
+    return RoundKernel::kShared;
+  return c.n > 16 ? RoundKernel::kPlanned : RoundKernel::kPhase;
 }
 
 // Steps of the standalone consensus error per workgroup: 8 (as the round
@@ -468,7 +497,8 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
     val = c->skip_val.data();
   }
   DeviceGuard guard(c->device);
-  const bool planned = use_planned_kernel(*c);
+  const RoundKernel kernel = pick_round_kernel(*c, rp, col, val, step != nullptr);
+  const bool planned = kernel == RoundKernel::kPlanned;
   int slots = 0;
   if (planned) {
     // rows with equal entries share their neighbour sum where it does not
@@ -480,7 +510,10 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
   }
   gasloc::LaunchShape shape;
   size_t lds = 0;
-  if (planned) {
+  if (kernel == RoundKernel::kShared) {
+    shape = gasloc::LaunchShape{gasloc::shared_vec(c->n, c->hp.param_dtype), 256, 0, 4, 0};
+    lds = gasloc::kStaticLds;
+  } else if (planned) {
     // 4 columns per thread when the plan needs few slots (n=64 1-Peer: 10.7-
     // 12.8 ms), else 2 (1 column was 25% slower).  The workgroup size is the
     // one that keeps the most waves resident per CU (LDS granules, registers;
@@ -523,8 +556,11 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
                                   &err))
       return fail(c, GASLOC_EINVAL, err);
   }
-  gasloc_status st = planned ? upload_plan(c, c->plan_ops) : upload_csr(c, rp, col, val, nnz);
-  if (st != GASLOC_OK) return st;
+  // the shared kernel takes row 0's weights as arguments, not from the device CSR
+  if (kernel != RoundKernel::kShared) {
+    gasloc_status st = planned ? upload_plan(c, c->plan_ops) : upload_csr(c, rp, col, val, nnz);
+    if (st != GASLOC_OK) return st;
+  }
 
   gasloc::GossipArgs a{};
   a.x = c->buf.x;
@@ -566,7 +602,13 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
   }
   a.partials = c->d_partials;
   a.pg_partials = c->d_partials + gasloc::kMaxPartials;
-  if (planned) {
+  if (kernel == RoundKernel::kShared) {
+    for (int32_t k = rp[0]; k < rp[1]; ++k) {
+      a.shared_mask |= 1ull << col[k];
+      a.shared_w[col[k]] = val[k];
+    }
+    HIP_TRY(c, gasloc::launch_gossip_shared(a, c->hp.param_dtype, step != nullptr, shape, c->stream));
+  } else if (planned) {
     a.ops = reinterpret_cast<const int32_t*>(c->d_csr);
     a.slots = slots;
     HIP_TRY(c, gasloc::launch_gossip_planned(a, c->hp.param_dtype, step != nullptr, c->hp.round_form, shape,

@@ -373,6 +373,49 @@ def test_explicit_csr_with_equal_rows(form, dtype):
     pair.check_state(tag="equal rows %s %s" % (form, dtype))
 
 
+@pytest.mark.parametrize("n,dtype,fused", [(3, "f32", False), (12, "bf16", True), (24, "bf16", False),
+                                           (33, "f32", True), (40, "bf16", False), (64, "f32", True),
+                                           (64, "bf16", True), (20, "bf16", True)])
+def test_rows_all_equal_share_one_running_sum(n, dtype, fused):
+    # every row holds the same entries (the complete graph, DiLoCo's average):
+    # the EQ round keeps one running sum per column and each row's own gamma
+    # term.  Shared rows that skip most workers (so most rows lack their own
+    # column), hold an explicit zero weight, or name every worker; the gamma
+    # term from the second round on; fused and standalone rounds (the fused
+    # bf16 round at 17-32 workers runs the planned kernel)
+    P = 5_003
+    log("case all rows equal n=%d %s fused=%s" % (n, dtype, fused))
+    rng = np.random.default_rng(n + 100 * (dtype == "bf16"))
+    pair = Pair(n, P, "ring", dtype, gamma=0.1)
+    for t in range(4):
+        if t == 0:
+            cols = list(range(n))
+            w = np.full(n, 1.0 / n)
+        elif t == 1:
+            cols = [0, min(1, n - 1)] if n > 1 else [0]
+            cols = sorted(set(cols))
+            w = np.full(len(cols), 1.0 / len(cols))
+        elif t == 2:
+            cols = sorted(set([0, n // 2, n - 1]))
+            w = np.zeros(len(cols))
+            w[0] = 0.5
+            w[-1] += 0.5  # the middle entry has weight 0 (an explicit zero)
+        else:
+            cols = sorted(rng.choice(n, size=max(1, n // 3), replace=False).tolist())
+            w = rng.random(len(cols)) + 0.1
+            w = w / w.sum()
+        W = _csr_from_rows([(cols, w)] * n)
+        if fused:
+            pair.local_step()
+            pair.local_step_gossip_round(t, W=W)
+        else:
+            pair.local_step()
+            pair.gossip_round(t, W=W)
+        reduction_close(pair.gpu.consensus_error(), pair.oracles["f32"].consensus_error(), "CE round %d" % t)
+    stats = pair.check_state(tag="all rows equal n=%d %s" % (n, dtype))
+    assert min(stats.values()) == 1.0, stats
+
+
 def _bf16_edge_pairs(rng, P):
     """Two rows of bf16 bit patterns whose fp32 midpoints meet the rounding
     cases: adjacent values (exact ties, both parities of the lower one), random
