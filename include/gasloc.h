@@ -61,12 +61,13 @@ typedef enum {
  * neighbourhoods are sets, and unless stated the weights are 1/|N_i|
  * (Algorithm 1's average over N_i).  Columns are ascending within a row.
  * Cost: every graph gives the same results at any n, but beyond 16 workers
- * the round keeps each column's live values in LDS, so graphs that need many
- * of them at once run well below the HBM rate: the complete graph (all n
- * live; rows share one sum) and the static exponential graph (28 to 64
- * live) at n = 32-64 ran at 31-58% of peak bandwidth, the sparse 1-Peer,
- * 2-Peer, ring and random 3-regular graphs at 69-77%.  Use dense graphs beyond
- * 16 workers for checks (the complete graph is DiLoCo), not for speed. */
+ * the round keeps each column's live values in LDS, so graphs whose distinct
+ * rows need many of them at once run well below the HBM rate: the static
+ * exponential graph (28 to 54 live) at n = 32-64 ran at 31-54% of peak
+ * bandwidth, the sparse 1-Peer, 2-Peer, ring and random 3-regular graphs at
+ * 69-77%.  Rows that are all the same (the complete graph, DiLoCo) share one
+ * running sum instead: 63-77% of peak in fp32, 40-75% in bf16.  Use the
+ * exponential graph beyond 16 workers for checks, not for speed. */
 typedef enum {
   GASLOC_TOPO_EXPLICIT = 0,       /* the caller passes W to every round            */
   GASLOC_TOPO_RING = 1,           /* static cycle {i-1, i, i+1} (Tables 1-3 "ring")  */

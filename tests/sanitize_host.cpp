@@ -40,6 +40,12 @@ void plan_and_verify(int n, const Csr& w, std::mt19937_64& rng, uint64_t t) {
     expect(ok, "plan_round", n, t);
     if (!ok) continue;
     expect(ops.size() <= gasloc::plan_words_max(n), "plan size bound", n, t);
+    // the kernel's form of the plan: slot words scaled to byte offsets
+    for (int32_t unit : {4, 1024, 4096}) {
+      std::vector<int32_t> scaled = ops;
+      expect(gasloc::scale_plan_slots(&scaled, unit, &err), "scale_plan_slots", n, t);
+      expect(scaled.size() == ops.size(), "scaled plan size", n, t);
+    }
     // corrupted copies must be rejected (or, if a change happens to keep the
     // plan valid, accepted) without reading out of bounds
     for (int trial = 0; trial < 20; ++trial) {

@@ -1,8 +1,8 @@
 """Host code and oracle under AddressSanitizer and UndefinedBehaviorSanitizer
 (CPU only).  The kernels own disjoint columns by construction, so the device
 side is covered by the bit-identity and padding tests; here the host side is:
-the library's schedule generators, visit planner and verifier (also on
-corrupted plans), skipped exchanges and LR schedule, and every round form of
+the library's schedule generators, visit planner, its verifier (also on
+corrupted plans) and the plan's scaling to byte offsets, skipped exchanges and LR schedule, and every round form of
 the oracle in both precisions.  Both are built with the host compilers and
 run as separate processes; any sanitizer report fails the test."""
 import os
