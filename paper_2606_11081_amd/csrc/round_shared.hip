@@ -21,6 +21,8 @@
 namespace gasloc {
 namespace {
 
+constexpr int kSharedBatch = 4;  // workers whose loads are issued together
+
 // Workers J0 .. J0 + R - 1 (those below n): their loads issued together,
 // then each one's value joins the shared sum (if its column is among the
 // entries) and leaves its row term.  J0 is a template argument so that every
@@ -136,7 +138,7 @@ __device__ __forceinline__ void shared_rows(const GossipArgs& a, int64_t p, int 
 template <int DT, int V, int NMAX, bool FUSED, int... B>
 __device__ __forceinline__ void shared_column(const GossipArgs& a, int64_t p, int cnt, double& ce, double& pg,
                                               std::integer_sequence<int, B...>) {
-  constexpr int R = 4;  // workers whose loads are issued together
+  constexpr int R = kSharedBatch;
   float sum[V], term[NMAX][V];
 #pragma unroll
   for (int c = 0; c < V; ++c) sum[c] = 0.0f;
@@ -159,7 +161,7 @@ __global__ __launch_bounds__(256) void k_gossip_shared(GossipArgs a) {
   for (int64_t gi = g_begin + threadIdx.x; gi < g_end; gi += nt) {
     const int64_t p = gi * V;
     const int cnt = static_cast<int>(a.P - p < V ? a.P - p : V);
-    shared_column<DT, V, NMAX, FUSED>(a, p, cnt, ce, pg, std::make_integer_sequence<int, NMAX / 4>{});
+    shared_column<DT, V, NMAX, FUSED>(a, p, cnt, ce, pg, std::make_integer_sequence<int, NMAX / kSharedBatch>{});
   }
   double total_ce, total_pg;
   block_sum2(ce, pg, total_ce, total_pg);
