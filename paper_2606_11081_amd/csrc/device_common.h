@@ -7,7 +7,8 @@
 // Every kernel streams [n, P] buffers once: the path is HBM-bandwidth bound
 // (well under 2 flop per byte), so the kernels use the vector ALU only (no
 // MFMA), 16-byte-per-lane loads and stores where the dtype allows, and a
-// grid-stride loop over column groups.
+// non-persistent grid whose workgroups take consecutive column tiles in
+// dispatch order.
 //
 // Floating-point contract: no contraction (each product and sum is rounded
 // on its own), correctly rounded fp32 division and square root (HIP's
