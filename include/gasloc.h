@@ -244,7 +244,9 @@ gasloc_status gasloc_consensus_error_cols(gasloc_ctx *ctx, int64_t p_begin, int6
  * device [n, ld] in param_dtype (gasloc_dtype), 16-byte aligned, ld *
  * sizeof(param) a multiple of 16; columns [p_begin, p_end), 0 <= p_begin <=
  * p_end <= ld, p_end < 2^31; out: device, one fp64, 8-byte aligned, written
- * on hip_stream (the call does not wait).  Same per-column arithmetic as
+ * on hip_stream (the call does not wait), which must belong to the GPU that is
+ * current on the calling thread (x and out live there, and so does the
+ * scratch the call uses).  Same per-column arithmetic as
  * gasloc_consensus_error_cols; on ranges of at least 8 * 16 * 256 steps of
  * 1024 fp32 (2048 bf16) columns per CU it groups the sums the same way too.
  * Scratch: a fixed 512 KiB + 128 B device array inside the library (one copy

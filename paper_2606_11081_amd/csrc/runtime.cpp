@@ -232,14 +232,18 @@ int resident_blocks_per_cu(const gasloc_ctx& c, const gasloc::LaunchShape& s, bo
 // P=350M from 26.9 to 25.6 ms and n=64, P=50M from 10.7 to 10.4 ms, while 64
 // was slower again (26.3, 10.8 ms).  So per = 8, less where that would leave
 // fewer than 16 workgroups per CU (n=4, P=1M: 0.031 ms at per = 1, 0.061 at
-// 8), and more only if the partials buffer requires it.
-void tile_grid(const gasloc_ctx& c, gasloc::LaunchShape* s) {
+// 8), and more only if the partials buffer requires it.  The planned kernel
+// with more than 8 slots (small LDS-bound workgroups, many of them per CU)
+// takes one step per workgroup: on the n=32 random 3-regular bf16 workload
+// 1-3% faster than 8 in each of three processes, round alone and fused.
+void tile_grid(const gasloc_ctx& c, gasloc::LaunchShape* s, int most_per) {
 #ifdef GASLOC_TUNING
   if (const char* env = std::getenv("GASLOC_GOSSIP_PER")) s->per = std::max(0, std::atoi(env));
 #endif
   const int64_t groups = (c.P + s->vec - 1) / s->vec;
   const int64_t steps = (groups + s->threads - 1) / s->threads;
-  int64_t per = s->per > 0 ? s->per : std::min<int64_t>(8, std::max<int64_t>(1, steps / (16 * int64_t(c.cus))));
+  int64_t per = s->per > 0 ? s->per
+                           : std::min<int64_t>(most_per, std::max<int64_t>(1, steps / (16 * int64_t(c.cus))));
   per = std::max<int64_t>(per, (steps + gasloc::kMaxPartials - 1) / gasloc::kMaxPartials);
   s->per = static_cast<int>(per);
   s->blocks = static_cast<int>(std::max<int64_t>(1, (steps + per - 1) / per));
@@ -548,7 +552,7 @@ gasloc_status run_round(gasloc_ctx* c, const gasloc_csr* W, uint64_t t, const St
     if (step && shape.batch == 8) shape.batch = 4;  // the fused kernel batches at most 4 workers
     lds = gasloc::gossip_lds_bytes(c->n, nnz, shape) + gasloc::kStaticLds;
   }
-  tile_grid(*c, &shape);
+  tile_grid(*c, &shape, planned && slots > 8 ? 1 : 8);
   if (lds > c->lds_per_block_max) return fail(c, GASLOC_EINVAL, "gossip shape exceeds the device's LDS per workgroup");
   if (planned) {  // slot words become byte offsets for this launch's shape
     std::string err;
