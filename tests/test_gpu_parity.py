@@ -416,6 +416,31 @@ def test_rows_all_equal_share_one_running_sum(n, dtype, fused):
     assert min(stats.values()) == 1.0, stats
 
 
+@pytest.mark.parametrize("n,P,dtype", [(16, 4_099, "f32"), (32, 1, "bf16"), (32, 2_051, "f32"), (17, 777, "bf16")])
+def test_rows_all_equal_with_partial_activity(n, P, dtype):
+    # the shared-row kernel at its register-array boundaries (16 and 32
+    # workers), a single column, and heterogeneous activity: some workers
+    # skip the fused step, one takes no local step at all (its y is its x)
+    log("case all rows equal, partial activity n=%d P=%d %s" % (n, P, dtype))
+    pair = Pair(n, P, "ring", dtype, gamma=0.1)
+    rng = np.random.default_rng(7 * n + P)
+    W = _csr_from_rows([(list(range(n)), np.full(n, 1.0 / n))] * n)
+    for t in range(3):
+        first = np.ones(n, np.uint8)
+        first[n // 3] = 0  # no local step this round
+        pair.local_step(active=first)
+        last = (rng.random(n) < 0.6).astype(np.uint8)
+        last[n // 3] = 0
+        if t % 2 == 0:
+            pair.local_step_gossip_round(t, active=last, W=W)
+        else:
+            pair.local_step(active=last)
+            pair.gossip_round(t, W=W)
+        reduction_close(pair.gpu.consensus_error(), pair.oracles["f32"].consensus_error(), "CE round %d" % t)
+    stats = pair.check_state(tag="all rows equal, partial activity n=%d %s" % (n, dtype))
+    assert min(stats.values()) == 1.0, stats
+
+
 def _bf16_edge_pairs(rng, P):
     """Two rows of bf16 bit patterns whose fp32 midpoints meet the rounding
     cases: adjacent values (exact ties, both parities of the lower one), random
