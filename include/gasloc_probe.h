@@ -8,9 +8,12 @@
  * vector: each thread reads 4 consecutive elements of every source stream,
  * adds them in fp32 and stores the sum to 4 consecutive elements of every
  * destination stream (bf16 streams rounded to nearest-even).  Workgroups of
- * 256 threads take one tile of 1024 elements each, dispatched in order, as
- * the round's kernels do.  Accesses are 16 bytes per lane for fp32 streams
- * and 8 for bf16 ones, non-temporal.
+ * `threads` threads take one tile of 4 * threads elements each, dispatched
+ * in order, as the round's kernels do.  Accesses are 16 bytes per lane for
+ * fp32 streams and 8 for bf16 ones, non-temporal.  Which workgroup size
+ * streams fastest depends on the mix (on MI355X, 64-thread workgroups are
+ * a few percent faster on some mixes and slower on others), so a caller
+ * after the achievable rate times several and keeps the fastest.
  */
 #ifndef GASLOC_PROBE_H
 #define GASLOC_PROBE_H
@@ -40,17 +43,17 @@ extern "C" {
  * ones; dst likewise.  A destination may be the same buffer as a source of the
  * same type (an in-place update, as in the round); otherwise streams must not
  * overlap.  Every pointer 16-byte aligned, each stream `count` elements,
- * count in [1, 2^31).  sink: device, at least 4 bytes; written only by a
+ * count in [1, 2^31).  threads: the workgroup size, 64, 128 or 256.  sink: device, at least 4 bytes; written only by a
  * read-only mix, and only where the sum of a thread's elements is a NaN whose
  * bits are 0x7fc0dead (so that the reads cannot be optimised away; finite
  * inputs never write it).
  * Enqueues one kernel on hip_stream (a hipStream_t; NULL = the null stream).
  * Errors: EINVAL for an unsupported mix, NULL or misaligned pointers, count
- * out of range; EDEVICE if the launch fails.  The message is given by
- * gasloc_last_error(NULL). */
+ * out of range, threads not 64, 128 or 256; EDEVICE if the launch fails.  The
+ * message is given by gasloc_last_error(NULL). */
 gasloc_status gasloc_stream_probe(int32_t reads_f32, int32_t reads_bf16, int32_t writes_f32,
                                   int32_t writes_bf16, const void *const *src, void *const *dst,
-                                  int64_t count, void *sink, void *hip_stream);
+                                  int64_t count, int32_t threads, void *sink, void *hip_stream);
 
 #ifdef __cplusplus
 }

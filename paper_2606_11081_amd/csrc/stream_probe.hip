@@ -1,6 +1,7 @@
 // Measurement support: a streaming kernel with the byte mix of a round
-// kernel (see gasloc_probe.h), launched like the round's kernels (one
-// 256-thread workgroup per tile of 1024 elements, in tile order).
+// kernel (see gasloc_probe.h), launched in tile order like the round's
+// kernels, one workgroup of 64, 128 or 256 threads per tile of 4 elements
+// per thread.
 #pragma clang fp contract(off)
 
 #include <string>
@@ -49,10 +50,11 @@ __global__ __launch_bounds__(256) void k_stream_probe(ProbeArgs a) {
 }
 
 template <int R32, int R16, int W32, int W16>
-hipError_t launch_probe(const ProbeArgs& a, hipStream_t stream) {
-  const int64_t tiles = (a.count + 1023) / 1024;
-  hipLaunchKernelGGL((k_stream_probe<R32, R16, W32, W16>), dim3(static_cast<unsigned>(tiles)), dim3(256), 0, stream,
-                     a);
+hipError_t launch_probe(const ProbeArgs& a, int threads, hipStream_t stream) {
+  const int64_t tile = 4 * static_cast<int64_t>(threads);
+  const int64_t tiles = (a.count + tile - 1) / tile;
+  hipLaunchKernelGGL((k_stream_probe<R32, R16, W32, W16>), dim3(static_cast<unsigned>(tiles)), dim3(threads), 0,
+                     stream, a);
   return hipGetLastError();
 }
 
@@ -61,7 +63,7 @@ hipError_t launch_probe(const ProbeArgs& a, hipStream_t stream) {
 
 extern "C" gasloc_status gasloc_stream_probe(int32_t reads_f32, int32_t reads_bf16, int32_t writes_f32,
                                              int32_t writes_bf16, const void* const* src, void* const* dst,
-                                             int64_t count, void* sink, void* hip_stream) {
+                                             int64_t count, int32_t threads, void* sink, void* hip_stream) {
   using gasloc::ProbeArgs;
   auto bad = [](const char* msg) {
     gasloc::set_thread_error(msg);
@@ -75,6 +77,7 @@ extern "C" gasloc_status gasloc_stream_probe(int32_t reads_f32, int32_t reads_bf
   for (int k : {4000, 30, 1010, 4030, 3020, 3121, 2221, 7050, 6040, 5241}) ok = ok || k == code;
   if (!ok) return bad("stream_probe: unsupported mix of streams");
   if (count < 1 || count >= (int64_t(1) << 31)) return bad("stream_probe: count outside [1, 2^31)");
+  if (threads != 64 && threads != 128 && threads != 256) return bad("stream_probe: threads must be 64, 128 or 256");
   if ((reads_f32 + reads_bf16 > 0 && !src) || (writes_f32 + writes_bf16 > 0 && !dst))
     return bad("stream_probe: NULL stream array");
   ProbeArgs a{};
@@ -94,16 +97,16 @@ extern "C" gasloc_status gasloc_stream_probe(int32_t reads_f32, int32_t reads_bf
   hipStream_t s = static_cast<hipStream_t>(hip_stream);
   hipError_t e = hipSuccess;
   switch (code) {
-    case 4000: e = gasloc::launch_probe<4, 0, 0, 0>(a, s); break;
-    case 30: e = gasloc::launch_probe<0, 0, 3, 0>(a, s); break;
-    case 1010: e = gasloc::launch_probe<1, 0, 1, 0>(a, s); break;
-    case 4030: e = gasloc::launch_probe<4, 0, 3, 0>(a, s); break;
-    case 3121: e = gasloc::launch_probe<3, 1, 2, 1>(a, s); break;
-    case 2221: e = gasloc::launch_probe<2, 2, 2, 1>(a, s); break;
-    case 3020: e = gasloc::launch_probe<3, 0, 2, 0>(a, s); break;
-    case 7050: e = gasloc::launch_probe<7, 0, 5, 0>(a, s); break;
-    case 6040: e = gasloc::launch_probe<6, 0, 4, 0>(a, s); break;
-    default: e = gasloc::launch_probe<5, 2, 4, 1>(a, s); break;
+    case 4000: e = gasloc::launch_probe<4, 0, 0, 0>(a, threads, s); break;
+    case 30: e = gasloc::launch_probe<0, 0, 3, 0>(a, threads, s); break;
+    case 1010: e = gasloc::launch_probe<1, 0, 1, 0>(a, threads, s); break;
+    case 4030: e = gasloc::launch_probe<4, 0, 3, 0>(a, threads, s); break;
+    case 3121: e = gasloc::launch_probe<3, 1, 2, 1>(a, threads, s); break;
+    case 2221: e = gasloc::launch_probe<2, 2, 2, 1>(a, threads, s); break;
+    case 3020: e = gasloc::launch_probe<3, 0, 2, 0>(a, threads, s); break;
+    case 7050: e = gasloc::launch_probe<7, 0, 5, 0>(a, threads, s); break;
+    case 6040: e = gasloc::launch_probe<6, 0, 4, 0>(a, threads, s); break;
+    default: e = gasloc::launch_probe<5, 2, 4, 1>(a, threads, s); break;
   }
   if (e != hipSuccess) {
     gasloc::set_thread_error(std::string("stream_probe: ") + hipGetErrorString(e));

@@ -84,7 +84,7 @@ _SIGNATURES = {
     "gasloc_set_counters": (ctypes.c_int, [_vp, _vp, _vp, _i64]),
     "gasloc_lr_schedule": (ctypes.c_float, [ctypes.c_float, _i64, _i64, ctypes.c_float, ctypes.c_float,
                                             ctypes.c_float]),
-    "gasloc_stream_probe": (ctypes.c_int, [_i32, _i32, _i32, _i32, _vp, _vp, _i64, _vp, _vp]),
+    "gasloc_stream_probe": (ctypes.c_int, [_i32, _i32, _i32, _i32, _vp, _vp, _i64, _i32, _vp, _vp]),
     "gasloc_last_error": (ctypes.c_char_p, [_vp]),
     "gasloc_build_info": (ctypes.c_char_p, []),
     "gasloc_destroy": (None, [_vp]),
@@ -307,15 +307,17 @@ def gasloc_lr_schedule(peak, step, total_steps, warmup_frac=0.1, start_frac=0.01
 
 
 def gasloc_stream_probe(reads_f32, reads_bf16, writes_f32, writes_bf16, src, dst, count, sink=None,
-                        stream=None):
+                        stream=None, threads=256):
     """Measurement support (include/gasloc_probe.h): one launch of the streaming
     kernel with the given byte mix.  src, dst: lists of torch device tensors
     (fp32 streams first, then bf16); sink: a device tensor of at least 4 bytes
-    for read-only mixes; stream: a torch stream (None = the null stream)."""
+    for read-only mixes; stream: a torch stream (None = the null stream);
+    threads: the workgroup size (64, 128 or 256)."""
     srcs = (ctypes.c_void_p * max(1, len(src)))(*[_dev(t) for t in src])
     dsts = (ctypes.c_void_p * max(1, len(dst)))(*[_dev(t) for t in dst])
     st = library().gasloc_stream_probe(int(reads_f32), int(reads_bf16), int(writes_f32), int(writes_bf16), srcs,
-                                       dsts, int(count), _dev(sink), None if stream is None else stream.cuda_stream)
+                                       dsts, int(count), int(threads), _dev(sink),
+                                       None if stream is None else stream.cuda_stream)
     _check(st)
 
 

@@ -49,8 +49,10 @@ int main(void) {
   printf("lr=%.9g %.9g %.9g\n", gasloc_lr_schedule(1e-3f, 0, 100, 0.1f, 0.01f, 0.0f),
          gasloc_lr_schedule(1e-3f, 10, 100, 0.1f, 0.01f, 0.0f), gasloc_lr_schedule(1e-3f, 99, 100, 0.1f, 0.01f, 0.0f));
 
-  /* rejected before any device work: a mix no kernel has, and a zero count */
-  printf("probe_mix=%d\n", (int)gasloc_stream_probe(1, 1, 1, 1, NULL, NULL, 1024, NULL, NULL));
-  printf("probe_count=%d\n", (int)gasloc_stream_probe(1, 0, 1, 0, NULL, NULL, 0, NULL, NULL));
+  /* rejected before any device work: a mix no kernel has, a zero count, a
+     workgroup size the probe does not launch */
+  printf("probe_mix=%d\n", (int)gasloc_stream_probe(1, 1, 1, 1, NULL, NULL, 1024, 256, NULL, NULL));
+  printf("probe_count=%d\n", (int)gasloc_stream_probe(1, 0, 1, 0, NULL, NULL, 0, 256, NULL, NULL));
+  printf("probe_threads=%d\n", (int)gasloc_stream_probe(1, 0, 1, 0, NULL, NULL, 1024, 96, NULL, NULL));
   return 0;
 }

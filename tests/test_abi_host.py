@@ -260,17 +260,20 @@ def test_skip_exchanges_on_a_csr_without_diagonal():
     assert list(got[0]) == [0, 2, 4, 5]
 
 
-@pytest.mark.parametrize("mix,count,msg", [
-    ((1, 1, 1, 1), 1024, "unsupported mix"),
-    ((4, 0, 3, 1), 1024, "unsupported mix"),
-    ((-1, 0, 1, 0), 1024, "unsupported mix"),
-    ((1, 0, 1, 0), 0, "count outside"),
-    ((1, 0, 1, 0), 1 << 31, "count outside"),
+@pytest.mark.parametrize("mix,count,threads,msg", [
+    ((1, 1, 1, 1), 1024, 256, "unsupported mix"),
+    ((4, 0, 3, 1), 1024, 256, "unsupported mix"),
+    ((-1, 0, 1, 0), 1024, 256, "unsupported mix"),
+    ((1, 0, 1, 0), 0, 256, "count outside"),
+    ((1, 0, 1, 0), 1 << 31, 256, "count outside"),
+    ((1, 0, 1, 0), 1024, 0, "threads must be"),
+    ((1, 0, 1, 0), 1024, 32, "threads must be"),
+    ((1, 0, 1, 0), 1024, 512, "threads must be"),
 ])
-def test_stream_probe_rejects_bad_arguments(mix, count, msg):
+def test_stream_probe_rejects_bad_arguments(mix, count, threads, msg):
     # every case fails before any device work
     lib = g.library()
-    st = lib.gasloc_stream_probe(*mix, None, None, count, None, None)
+    st = lib.gasloc_stream_probe(*mix, None, None, count, threads, None, None)
     assert st == g.gasloc.GASLOC_EINVAL
     assert msg in g.gasloc.gasloc_last_error(None)
 
@@ -279,13 +282,13 @@ def test_stream_probe_rejects_null_and_misaligned_streams():
     lib = g.library()
     src = (ctypes.c_void_p * 1)(None)
     dst = (ctypes.c_void_p * 1)(0x1000)
-    assert lib.gasloc_stream_probe(1, 0, 1, 0, src, dst, 64, None, None) == g.gasloc.GASLOC_EINVAL
+    assert lib.gasloc_stream_probe(1, 0, 1, 0, src, dst, 64, 256, None, None) == g.gasloc.GASLOC_EINVAL
     assert "source" in g.gasloc.gasloc_last_error(None)
     src = (ctypes.c_void_p * 1)(0x1008)
-    assert lib.gasloc_stream_probe(1, 0, 1, 0, src, dst, 64, None, None) == g.gasloc.GASLOC_EINVAL
+    assert lib.gasloc_stream_probe(1, 0, 1, 0, src, dst, 64, 256, None, None) == g.gasloc.GASLOC_EINVAL
     assert "misaligned" in g.gasloc.gasloc_last_error(None)
     src = (ctypes.c_void_p * 4)(0x1000, 0x2000, 0x3000, 0x4000)
-    assert lib.gasloc_stream_probe(4, 0, 0, 0, src, None, 64, None, None) == g.gasloc.GASLOC_EINVAL
+    assert lib.gasloc_stream_probe(4, 0, 0, 0, src, None, 64, 256, None, None) == g.gasloc.GASLOC_EINVAL
     assert "sink" in g.gasloc.gasloc_last_error(None)
 
 

@@ -42,6 +42,7 @@ def test_plain_c_consumer(tmp_path):
     assert [np.float32(v) for v in lr] == [np.float32(v) for v in expect]
     assert lines["probe_mix"] == "1"    # GASLOC_EINVAL: unsupported mix of streams
     assert lines["probe_count"] == "1"  # GASLOC_EINVAL: count outside [1, 2^31)
+    assert lines["probe_threads"] == "1"  # GASLOC_EINVAL: threads not 64, 128 or 256
 
 
 @pytest.mark.gpu

@@ -23,13 +23,14 @@ def _bf16_bits(a):
 
 @pytest.mark.parametrize("mix", MIXES)
 @pytest.mark.parametrize("in_place", [False, True])
-def test_probe_mix_stores_the_sum(mix, in_place):
+@pytest.mark.parametrize("threads", [256, 128, 64])
+def test_probe_mix_stores_the_sum(mix, in_place, threads):
     import torch
 
     r32, r16, w32, w16 = mix
-    count = 5 * 1024 + 7  # several tiles and a ragged tail
-    print("case probe mix %s in_place=%s count=%d" % (mix, in_place, count), flush=True)
-    gen = torch.Generator(device="cpu").manual_seed(sum(mix) * 7 + int(in_place))
+    count = 5 * 1024 + 7  # several tiles (of every workgroup size) and a ragged tail
+    print("case probe mix %s in_place=%s count=%d threads=%d" % (mix, in_place, count, threads), flush=True)
+    gen = torch.Generator(device="cpu").manual_seed(sum(mix) * 7 + int(in_place) + threads)
     src32 = [torch.randn(count, generator=gen).cuda() for _ in range(r32)]
     src16 = [torch.randn(count, generator=gen).to(torch.bfloat16).cuda() for _ in range(r16)]
     expect = np.zeros(count, np.float32)
@@ -42,7 +43,7 @@ def test_probe_mix_stores_the_sum(mix, in_place):
         dst32 = [torch.zeros(count).cuda() for _ in range(w32)]
         dst16 = [torch.zeros(count, dtype=torch.bfloat16).cuda() for _ in range(w16)]
     sink = torch.zeros(1, dtype=torch.int32, device="cuda")
-    g.gasloc.gasloc_stream_probe(r32, r16, w32, w16, src32 + src16, dst32 + dst16, count, sink)
+    g.gasloc.gasloc_stream_probe(r32, r16, w32, w16, src32 + src16, dst32 + dst16, count, sink, threads=threads)
     torch.cuda.synchronize()
     for t in dst32:
         assert np.array_equal(t.cpu().numpy().view(np.uint32), expect.view(np.uint32))
