@@ -65,7 +65,8 @@ typedef enum {
  * rows need many of them at once run well below the HBM rate: the static
  * exponential graph (28 to 54 live) at n = 32-64 ran at 31-54% of peak
  * bandwidth, the sparse 1-Peer, 2-Peer, ring and random 3-regular graphs at
- * 69-77%.  Rows that are all the same (the complete graph, DiLoCo) share one
+ * 63-77% (the low end where the buffers' physical placement is unfavourable:
+ * the same round on other allocations runs at the high end).  Rows that are all the same (the complete graph, DiLoCo) share one
  * running sum instead: 63-77% of peak in fp32, 40-75% in bf16.  Use the
  * exponential graph beyond 16 workers for checks, not for speed. */
 typedef enum {
