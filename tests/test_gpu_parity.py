@@ -68,6 +68,30 @@ def test_ring_n4_p1m_full_state_ten_rounds():
     assert np.array_equal(out.cpu().numpy().view(np.uint32), ref.view(np.uint32))
 
 
+@pytest.mark.parametrize("n,P,topology,dtype", [(5, 9_999, "two_peer", "bf16"), (37, 5_003, "one_peer", "f32"),
+                                                  (64, 2_051, "complete", "bf16"), (16, 1, "ring", "f32")])
+def test_replica_mean_matches_the_oracle(n, P, topology, dtype):
+    # the network average (Algorithm 1's output) after rounds that leave the
+    # replicas apart: fp32 bits, or bf16 bits rounded from the fp32 mean, as
+    # the fp32 oracle stores them; ragged P, odd n, and a single column
+    import torch
+
+    log("case replica mean n=%d P=%d %s %s" % (n, P, topology, dtype))
+    pair = Pair(n, P, topology, dtype, gamma=0.1)
+    for t in range(2):
+        pair.local_step()
+        pair.gossip_round(t)
+    out = torch.empty(P, dtype=torch.bfloat16 if dtype == "bf16" else torch.float32, device="cuda")
+    pair.gpu.replica_mean(out)
+    torch.cuda.synchronize()
+    ref = pair.oracles["f32"].replica_mean()
+    if dtype == "bf16":
+        got = out.view(torch.int16).cpu().numpy().view(np.uint16)
+        assert np.array_equal(got, np.asarray(ref).view(np.uint16))
+    else:
+        assert np.array_equal(out.cpu().numpy().view(np.uint32), np.asarray(ref).view(np.uint32))
+
+
 SMALL = [
     # n, P, topology, dtype, H, gamma, mu, nesterov
     (1, 1000, "ring", "f32", 2, 0.1, 0.9, True),
