@@ -613,23 +613,27 @@ def test_pseudo_gradient_statistic_zero_cases(n, topology):
     assert pair.gpu.pseudo_gradient_sq() == 0.0
 
 
-def test_consensus_error_columns_and_closed_form():
+@pytest.mark.parametrize("n,topology,dtype", [(16, "one_peer_exp", "f32"), (32, "random_regular", "bf16")])
+def test_consensus_error_columns_and_closed_form(n, topology, dtype):
+    # the standalone reduction over column ranges that start and end off the
+    # 16-byte column groups (4 fp32 or 8 bf16 columns), against the oracle
     import torch
 
-    n, P = 16, 1_000_003
-    pair = Pair(n, P, "one_peer_exp", "f32", precisions=("f32",))
+    P = 1_000_003
+    log("case consensus error columns n=%d %s %s" % (n, topology, dtype))
+    pair = Pair(n, P, topology, dtype, precisions=("f32",))
     pair.local_step()
     pair.gossip_round(0)
     fused = pair.gpu.consensus_error()
     total = pair.gpu.consensus_error_cols(0, P)
     reduction_close(total, fused, "standalone vs fused")
     o = pair.oracles["f32"]
-    for a, b in [(0, 1), (0, 4097), (5, 70_001), (P - 999, P), (123_456, 123_456)]:
+    for a, b in [(0, 1), (0, 4097), (5, 70_001), (3, 11), (P - 999, P), (P - 5, P), (123_456, 123_456)]:
         got = pair.gpu.consensus_error_cols(a, b)
         reduction_close(got, o.consensus_error(slice(a, b)) if b > a else 0.0, "cols [%d,%d)" % (a, b))
     # closed form: x_i = c_i on every column -> CE = P * sum_i (c_i - cbar)^2 exactly
-    c = torch.arange(1, n + 1, dtype=torch.float32, device="cuda").view(n, 1)
-    pair.gpu.x[:, :P].copy_(c.expand(n, P))
+    c = torch.arange(1, n + 1, dtype=torch.float32, device="cuda").view(n, 1)  # exact in bf16 too
+    pair.gpu.x[:, :P].copy_(c.expand(n, P).to(pair.gpu.x.dtype))
     expect = P * float(((np.arange(1, n + 1) - (n + 1) / 2.0) ** 2).sum())
     assert pair.gpu.consensus_error_cols(0, P) == expect
 
