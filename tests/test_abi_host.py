@@ -135,6 +135,82 @@ def test_validate_csr_rejects(case):
         g.gasloc_validate_csr((rp, col, val), n)
 
 
+def _csr_is_valid(rp, col, val, n):
+    """The documented acceptance rule of a caller's CSR (include/gasloc.h), restated."""
+    if len(rp) - 1 != n:
+        return False
+    nnz = len(col)
+    if nnz < n or nnz > n * n or rp[0] != 0 or rp[n] != nnz:
+        return False
+    for i in range(n):
+        b, e = int(rp[i]), int(rp[i + 1])
+        if e < b or b < 0 or e > nnz:
+            return False
+        total = 0.0
+        for k in range(b, e):
+            c = int(col[k])
+            if c < 0 or c >= n or (k > b and c <= int(col[k - 1])) or not np.isfinite(val[k]):
+                return False
+            total += float(val[k])  # fp64 sum of the fp32 weights, in CSR order
+        if abs(total - 1.0) > 1e-6:
+            return False
+    return True
+
+
+def test_validate_csr_agrees_with_its_rule_on_random_graphs():
+    # random row-stochastic CSRs, half of them with one random defect (or a
+    # weight nudged across the 1e-6 row-sum tolerance): the library accepts
+    # exactly those the documented rule accepts
+    rng = np.random.default_rng(2024)
+    decisions = {True: 0, False: 0}
+    for case in range(1500):
+        n = int(rng.integers(1, 13))
+        rows_c, rows_v = [], []
+        for i in range(n):
+            k = int(rng.integers(1, n + 1))
+            c = np.sort(rng.choice(n, size=k, replace=False)).astype(np.int32)
+            w = rng.random(k) + 0.05
+            w = (w / w.sum()).astype(np.float32)
+            w[-1] = np.float32(1.0 - float(np.sum(w[:-1], dtype=np.float64)))  # row sum close to 1 in fp64
+            rows_c.append(c)
+            rows_v.append(w)
+        rp = np.zeros(n + 1, np.int32)
+        rp[1:] = np.cumsum([len(c) for c in rows_c])
+        col = np.concatenate(rows_c).astype(np.int32)
+        val = np.concatenate(rows_v).astype(np.float32)
+        nv = n
+        if rng.random() < 0.5:
+            kind = int(rng.integers(0, 9))
+            k = int(rng.integers(0, len(col)))
+            if kind == 0 and len(col) > 1:
+                col[k], col[(k + 1) % len(col)] = col[(k + 1) % len(col)], col[k]
+            elif kind == 1:
+                col[k] = n + int(rng.integers(0, 3))
+            elif kind == 2:
+                col[k] = -1 - int(rng.integers(0, 3))
+            elif kind == 3:
+                val[k] = np.float32(val[k] + rng.choice([5e-7, -5e-7, 2e-6, -2e-6, 0.25]))
+            elif kind == 4:
+                val[k] = rng.choice([np.nan, np.inf, -np.inf])
+            elif kind == 5 and n > 1:
+                j = int(rng.integers(1, n))
+                rp[j] = rp[j] + int(rng.choice([-2, -1, 1, 2]))
+            elif kind == 6:
+                rp[-1] += int(rng.choice([-1, 1]))
+            elif kind == 7:
+                nv = n + 1 if n < 64 else n - 1
+            elif kind == 8 and len(col) > 1:
+                col[k] = col[k - 1] if k > 0 else col[1]
+        want = _csr_is_valid(rp, col, val, nv)
+        decisions[want] += 1
+        if want:
+            g.gasloc_validate_csr((rp, col, val), nv)
+        else:
+            with pytest.raises(g.GaslocError, match="EINVAL"):
+                g.gasloc_validate_csr((rp, col, val), nv)
+    assert decisions[True] > 300 and decisions[False] > 300, decisions
+
+
 def test_row_sum_tolerance_is_1e6_in_fp64():
     rp = np.array([0, 1], np.int32)
     col = np.array([0], np.int32)
