@@ -776,6 +776,43 @@ def test_full_size_sampled(name, sample, rounds):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("form", ["alg1", "dadam", "local_dadam"])
+def test_full_size_sampled_round_forms(form):
+    # the other round forms at the n=64, P=50M matching workload's full size,
+    # as the benchmark runs them (gamma = 0; Algorithm 1 with the last local
+    # step fused into the round, the DAdam forms as separate calls): 2^16
+    # sampled columns against both oracles, the full-size CE two ways
+    import torch
+
+    w = gi.WORKLOADS["matching-n64-p50m-hetH"]
+    log("case %s %s (sampled 65536 columns, 2 rounds)" % (w.name, form))
+    cols = gi.sample_columns(w.P, 1 << 16)
+    pair = Pair(w.n, w.P, w.topology, w.param_dtype, gamma=0.0, degree=w.degree, cols=cols, form=form)
+    H_i = gi.local_steps(w)
+    fuse = form == "alg1"
+    for t in range(2):
+        last = int(H_i.max()) - (1 if fuse else 0)
+        for h in range(last):
+            pair.local_step(active=(H_i > h).astype(np.uint8))
+        if fuse:
+            pair.local_step_gossip_round(t, active=(H_i > last).astype(np.uint8))
+        else:
+            pair.gossip_round(t)
+        ce = pair.gpu.consensus_error()
+        assert np.isfinite(ce) and ce >= 0.0
+        whole = pair.gpu.consensus_error_cols(0, w.P)
+        assert abs(whole - ce) <= 1e-10 * ce, (whole, ce)
+        o = pair.oracles["f32"]
+        reduction_close(pair.gpu.consensus_error_cols(0, 64), o.consensus_error(slice(0, 64)), "CE head")
+        reduction_close(pair.gpu.consensus_error_cols(w.P - 64, w.P),
+                        o.consensus_error(slice(len(cols) - 64, len(cols))), "CE tail")
+        log("round %d: CE %.6e" % (t, ce))
+    stats = pair.check_state(tag="%s %s" % (w.name, form))
+    log("bit-exact fraction vs fp32 oracle: %s" % stats)
+    del pair
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_extreme_gradients_bit_exact(dtype):
     # IEEE behaviour the op order relies on: subnormal squares (g ~ 1e-20 gives
