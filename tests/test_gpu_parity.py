@@ -776,6 +776,32 @@ def test_full_size_sampled(name, sample, rounds):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("n,P,dtype", [(16, 350_000_000, "f32"), (64, 50_000_000, "f32"), (32, 150_000_000, "bf16")])
+def test_full_size_sampled_two_peer(n, P, dtype):
+    # the paper's randomized 2-Peer cycle (section 3.2) at the workloads'
+    # sizes: H = 3, the last step fused, gamma = 0.1; 2^16 sampled columns
+    import torch
+
+    log("case two_peer n=%d P=%d %s (sampled 65536 columns, 3 rounds)" % (n, P, dtype))
+    cols = gi.sample_columns(P, 1 << 16)
+    pair = Pair(n, P, "two_peer", dtype, gamma=0.1, cols=cols,
+                precisions=("f32",) if dtype == "bf16" else ("f32", "f64"))
+    for t in range(3):
+        for _ in range(2):
+            pair.local_step()
+        pair.local_step_gossip_round(t)
+        ce = pair.gpu.consensus_error()
+        whole = pair.gpu.consensus_error_cols(0, P)
+        assert abs(whole - ce) <= 1e-10 * ce, (whole, ce)
+        o = pair.oracles["f32"]
+        reduction_close(pair.gpu.consensus_error_cols(P - 64, P),
+                        o.consensus_error(slice(len(cols) - 64, len(cols))), "CE tail")
+    stats = pair.check_state(tag="two_peer n=%d %s" % (n, dtype))
+    log("bit-exact fraction vs fp32 oracle: %s" % stats)
+    del pair
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("form", ["alg1", "dadam", "local_dadam"])
 def test_full_size_sampled_round_forms(form):
     # the other round forms at the n=64, P=50M matching workload's full size,
