@@ -12,7 +12,7 @@ pytestmark = pytest.mark.gpu
 
 KINDS = ["ring", "complete", "exponential", "one_peer_exp", "one_peer", "two_peer", "random_regular"]
 FORMS = ["eq", "eq", "eq", "alg1", "dadam", "local_dadam"]
-CASES = 48
+CASES = 96
 
 
 def draw(case):
